@@ -1,0 +1,207 @@
+"""Benchmark of the RadixAttention hot path on one MI355X.
+
+One step = one pass of the whole hot path over one continuous batch: store the
+batch's new tokens' K/V into their pool slots, extend attention for the
+extend requests, decode attention (partial pass + combine) for the decode
+requests.  The slot tables come from the native radix cache after replaying
+the workload's request history (host time reported separately).
+
+Default workload: the continuous-batching mix with 70B-like heads (64 query
+heads, 8 kv heads, head dim 128): 32 extend requests (cached prefix
+U[1024, 8192], extend U[256, 2048]) and 512 decode requests (context
+U[1024, 16384]) over a 4,194,304-slot pool, tables built by ~100k tree calls.
+
+Prints one JSON line.  Per-kernel durations come from HIP events recorded on
+the stream the kernels run on, inside the timed loop.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+BF16_PEAK_TFLOPS = 2500.0
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def algorithmic_work(sc, inp):
+    """Algorithmic flops of extend and bytes of decode for one step.
+
+    Extend: 4*D flops (QK^T and PV) per unmasked (query head, query, key)
+    triple: Hq * sum_r (E_r * P_r + E_r (E_r + 1) / 2).
+    Decode: each request reads K and V rows of its kv heads for all L_r
+    positions (2 * Hkv * D * 2 bytes), its slot index (4 bytes), its query
+    and writes its output (2 * Hq * D * 2 bytes).
+    """
+    hq, hkv, d = sc.hq, sc.hkv, sc.d
+    pairs = sum(e * p + e * (e + 1) // 2 for _, p, e, _ in inp.ext_meta)
+    ext_flops = 4.0 * d * hq * pairs
+    ext_bytes = sum((p + e) * (2 * hkv * d * 2) + p * 4 + e * (2 * hq * d * 2) for _, p, e, _ in inp.ext_meta)
+    sum_l = sum(l for _, l in inp.dec_meta)
+    dec_bytes = sum_l * (2 * hkv * d * 2 + 4) + inp.n_dec * 2 * hq * d * 2
+    dec_flops = 4.0 * d * hq * sum_l
+    attended = sum(p + e for _, p, e, _ in inp.ext_meta) + sum_l
+    return dict(ext_flops=ext_flops, ext_bytes=ext_bytes, dec_bytes=dec_bytes, dec_flops=dec_flops,
+                attended=attended, sum_l=sum_l, pairs=pairs)
+
+
+def cpu_baseline(sc, inp, budget_s: float):
+    """The oracle, timed on host cores over a bounded sample of the batch."""
+    from oracle import attention as oa
+
+    try:
+        from threadpoolctl import threadpool_info
+        blas_threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        blas_threads = 1
+    cores = len(os.sched_getaffinity(0))
+    done_tokens = 0
+    t_start = time.perf_counter()
+    n_ext = n_dec = 0
+    # one extend request (the shortest) then decode requests until the budget is spent
+    if inp.ext_meta:
+        toks, p, e, _ = min(inp.ext_meta, key=lambda m: m[2] * (m[1] + m[2]))
+        oa.extend_reference(toks, p, e, sc.seed, sc.hq, sc.hkv, sc.d, sc.scale)
+        done_tokens += p + e
+        n_ext += 1
+    for toks, l in inp.dec_meta:
+        if time.perf_counter() - t_start > budget_s:
+            break
+        oa.decode_reference(toks, l, sc.seed, sc.hq, sc.hkv, sc.d, sc.scale)
+        done_tokens += l
+        n_dec += 1
+    dt = time.perf_counter() - t_start
+    return {"value": done_tokens / dt, "unit": "attended KV tokens/s", "cores": max(cores, blas_threads),
+            "kind": "oracle",
+            "sample": f"{n_ext} extend + {n_dec} decode requests of the batch "
+                      f"({done_tokens} context tokens, {dt:.1f} s, inputs regenerated inside the timing)"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="mixed")
+    ap.add_argument("--cpu-budget", type=float, default=20.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for {args.gpus}); the path shards by request, "
+              f"see the design notes", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2312_07104_amd as pa
+    from tests.harness import ScenarioRun
+    from workload import scenarios as S
+
+    sc = S.ALL[args.workload]()
+    log(f"[bench] workload={sc.name} seed={sc.seed} Hq={sc.hq} Hkv={sc.hkv} D={sc.d} S={sc.pool_slots}")
+    run = ScenarioRun(sc)
+    log(f"[bench] history: {sc.history_len} requests, {run.history_ops} tree calls, {run.history_seconds:.2f} s")
+    inp = run.prepare(0)
+    log(f"[bench] batch planned: {run.plan_seconds * 1e3:.1f} ms host, hit rate {inp.plan.hit_rate:.3f}")
+    run.store(inp)  # the first pass writes new tokens' K/V (identical values every step)
+    torch.cuda.synchronize()
+    work = algorithmic_work(sc, inp)
+
+    stream = torch.cuda.current_stream()
+    n_new = inp.new_slots.shape[0]
+    ws_bytes = pa.ra_decode_workspace_bytes(inp.n_dec, sc.hq, sc.hkv, sc.d, inp.max_seq_len, 0)
+    workspace = torch.empty(max(ws_bytes, 16), dtype=torch.uint8, device="cuda")
+    out_e = torch.empty_like(inp.q_ext) if inp.n_ext else None
+    out_d = torch.empty_like(inp.q_dec) if inp.n_dec else None
+
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record(stream)
+        if n_new:
+            pa.ra_store_kv(inp.new_slots, inp.k_new, inp.v_new, run.k_pool, run.v_pool)
+        if ev is not None:
+            ev[1].record(stream)
+        if inp.n_ext:
+            run.extend(inp, out=out_e)
+        if ev is not None:
+            ev[2].record(stream)
+        if inp.n_dec:
+            run.decode(inp, workspace=workspace, out=out_d)
+        if ev is not None:
+            ev[3].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(events[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_step = wall * 1e3 / args.steps
+    t_store = float(np.mean([e[0].elapsed_time(e[1]) for e in events]))
+    t_ext = float(np.mean([e[1].elapsed_time(e[2]) for e in events]))
+    t_dec = float(np.mean([e[2].elapsed_time(e[3]) for e in events]))
+
+    kernels = {
+        "store_kv": {"ms": t_store, "tokens": int(n_new)},
+        "extend": {"ms": t_ext, "tflops": work["ext_flops"] / (t_ext * 1e-3) / 1e12 if t_ext else None,
+                   "flops": work["ext_flops"]},
+        "decode": {"ms": t_dec, "gbs": work["dec_bytes"] / (t_dec * 1e-3) / 1e9 if t_dec else None,
+                   "bytes": work["dec_bytes"]},
+    }
+    if inp.n_ext and t_ext >= t_dec:
+        ach = work["ext_flops"] / (t_ext * 1e-3) / 1e12
+        roof = {"kernel": "extend", "bound": "mfma", "achieved": ach, "peak": BF16_PEAK_TFLOPS,
+                "unit": "TFLOP/s", "frac": ach / BF16_PEAK_TFLOPS, "traffic": None}
+    else:
+        ach = work["dec_bytes"] / (t_dec * 1e-3) / 1e9
+        roof = {"kernel": "decode", "bound": "hbm", "achieved": ach, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": ach / HBM_PEAK_GBS, "traffic": None}
+    # second roofline line for the other kernel, same definitions
+    other = ({"kernel": "decode", "bound": "hbm", "achieved": kernels["decode"]["gbs"], "peak": HBM_PEAK_GBS,
+              "unit": "GB/s"} if roof["kernel"] == "extend" else
+             {"kernel": "extend", "bound": "mfma", "achieved": kernels["extend"]["tflops"],
+              "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s"})
+    if other["achieved"] is not None:
+        other["frac"] = other["achieved"] / other["peak"]
+
+    value = work["attended"] / (ms_step * 1e-3)
+    line = {
+        "metric": "attended KV tokens/s (extend + decode step over the radix-cached KV pool)",
+        "value": value, "unit": "attended KV tokens/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms_step, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": sc.name, "hq": sc.hq, "hkv": sc.hkv, "head_dim": sc.d,
+                   "pool_slots": sc.pool_slots, "extend_requests": inp.n_ext, "decode_requests": inp.n_dec,
+                   "sum_extend_tokens": inp.total_ext, "sum_decode_context": work["sum_l"],
+                   "history_requests": sc.history_len, "tree_calls": run.history_ops,
+                   "hit_rate": inp.plan.hit_rate, "parallelism": "none (1 GPU)"},
+        "roofline": roof,
+        "roofline_other": other,
+        "kernels": kernels,
+        "host_tree": {"calls": run.history_ops, "seconds": run.history_seconds,
+                      "calls_per_s": run.history_ops / max(run.history_seconds, 1e-9),
+                      "plan_batch_ms": run.plan_seconds * 1e3},
+    }
+    if not args.no_cpu_baseline:
+        log("[bench] timing the oracle on host cores")
+        line["cpu_baseline"] = cpu_baseline(sc, inp, args.cpu_budget)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

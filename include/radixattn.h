@@ -1,0 +1,177 @@
+/*
+ * radixattn.h -- C ABI of the RadixAttention hot path on MI355X (gfx950).
+ *
+ * Two halves:
+ *
+ *  1. Host radix cache (section 3 of the SGLang paper, "RadixAttention", and
+ *     Algorithm 1, cache-aware scheduling with continuous batching): a radix
+ *     tree mapping token sequences to slots of a token-granular KV pool (one
+ *     token per page), reference counters that protect what running requests
+ *     use, LRU eviction of unreferenced leaves, and the shared slot pool.
+ *     Not thread-safe per handle: one scheduler thread drives it, as the paper
+ *     keeps the tree on the CPU.
+ *
+ *  2. Device attention over that pool.  K and V live in two caller-owned
+ *     device arrays [S, Hkv, D] (bf16, row-major); request r reads position j
+ *     of its context from slot req_to_token[req_pool_idx[r] * rtt_stride + j].
+ *     extend: prefill of new tokens over a cached prefix plus causal attention
+ *     among themselves.  decode: one query token per request over its whole
+ *     context.  Every device call is asynchronous on the caller's HIP stream
+ *     and allocates no device memory; all pointers are device pointers unless
+ *     stated.  Results match float64 softmax attention (see the oracle) within
+ *     bf16 rounding.
+ *
+ * Conventions.  Tokens and slots are int32 (S < 2^31).  Host lengths are
+ * int64.  Node handles are int64 ids; the root is 0; ids are never reused.
+ * Every call returns RA_OK or a negative status and never throws; the text of
+ * the last error on the calling thread is available from ra_last_error().  A
+ * failing call changes nothing.  Query head h uses key/value head
+ * h / (Hq / Hkv) (contiguous groups).
+ */
+#ifndef RADIXATTN_H
+#define RADIXATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+  RA_OK = 0,
+  RA_EINVAL = -1, /* bad argument, unknown node, counter underflow, bad slot */
+  RA_ENOMEM = -2, /* pool has fewer free slots than asked (host, no effect) */
+  RA_EHIP = -3    /* a HIP launch failed; message holds hipGetErrorString */
+};
+
+/* Message for the last non-OK status returned on this thread ("" if none). */
+const char* ra_last_error(void);
+
+/* ===================================================================== */
+/* Host radix cache (section 3; Algorithm 1).                            */
+/* ===================================================================== */
+
+typedef struct ra_cache ra_cache;
+
+/* Creates a cache over a pool of `pool_slots` slots.  The free slots form a
+ * FIFO queue initialised to `initial_free_order` (a permutation of
+ * [0, pool_slots), copied), or to 0, 1, ... when it is NULL.  EINVAL if the
+ * order is not a permutation. */
+int ra_cache_create(int64_t pool_slots, const int32_t* initial_free_order, ra_cache** out);
+void ra_cache_destroy(ra_cache* c);
+
+/* Longest cached prefix of tokens[0..n) (Algorithm 1, match_prefix).
+ * Writes its slots to out_slots (capacity n; may be NULL), its length to
+ * *out_len and the node covering exactly that prefix to *out_node (0 when
+ * nothing matches).  A match ending inside an edge splits it there.  Every
+ * node on the walked path becomes most recently used. */
+int ra_match_prefix(ra_cache* c, const int32_t* tokens, int64_t n, int32_t* out_slots,
+                    int64_t* out_len, int64_t* out_node);
+
+/* Lock / unlock the root-to-node path for a running request (section 3:
+ * a node with a non-zero counter is never evicted).  *out_delta receives the
+ * change of the evictable token count: <= 0 for inc, >= 0 for dec (Algorithm
+ * 1 adds it to the available size).  dec on a path with a zero counter is
+ * EINVAL.  out_delta may be NULL. */
+int ra_inc_ref(ra_cache* c, int64_t node, int64_t* out_delta);
+int ra_dec_ref(ra_cache* c, int64_t node, int64_t* out_delta);
+
+/* Pool (Algorithm 1, P.alloc).  Pops n slots from the front of the free queue
+ * into out_slots, or returns ENOMEM with no effect if fewer are free. */
+int ra_alloc_slots(ra_cache* c, int64_t n, int32_t* out_slots);
+/* Appends slots to the free queue in order.  EINVAL (no effect) if any slot
+ * is out of range, already free, or repeated. */
+int ra_free_slots(ra_cache* c, const int32_t* slots, int64_t n);
+
+/* Inserts a finished sequence tokens[0..n) -> slots[0..n) (Algorithm 1,
+ * T.insert).  Cached positions keep their slots; a caller slot that differs
+ * from the cached one at the same position is returned to the pool.  Splits
+ * an edge where the sequence diverges inside it.  *out_cached = positions
+ * that were already cached, *out_node = node ending at position n (either may
+ * be NULL).  The new leaf is unreferenced (evictable). */
+int ra_insert(ra_cache* c, const int32_t* tokens, const int32_t* slots, int64_t n,
+              int64_t* out_cached, int64_t* out_node);
+
+/* Evicts least recently used unreferenced leaves (ties: smaller node id)
+ * until at least n_tokens slots were freed or nothing is evictable; whole
+ * leaves only, so it may free more.  Freed slots join the back of the free
+ * queue.  *out_freed = slots freed (may be NULL). */
+int ra_evict(ra_cache* c, int64_t n_tokens, int64_t* out_freed);
+
+int64_t ra_evictable_size(const ra_cache* c); /* tokens in unreferenced nodes */
+int64_t ra_available_size(const ra_cache* c); /* free slots */
+int64_t ra_cached_tokens(const ra_cache* c);  /* tokens held by the tree */
+int64_t ra_num_nodes(const ra_cache* c);      /* live nodes, root included */
+
+/* Canonical dump for exact comparisons: [clock, n_nodes, n_free, then per
+ * live node in id order: id, parent (-1 for root), ref, stamp, len, len
+ * tokens, len slots; then the free queue front to back].  *out_len gets the
+ * number of int64 words; with buf == NULL only the length is reported;
+ * EINVAL if cap is too small. */
+int ra_snapshot(const ra_cache* c, int64_t* buf, int64_t cap, int64_t* out_len);
+
+/* ===================================================================== */
+/* Device: KV pool and attention (gfx950 HIP kernels).                   */
+/* ===================================================================== */
+
+/* Scatter of new tokens' K and V into their pool slots (page size one,
+ * section 3): k_pool[slots[i]] = k_new[i], v_pool[slots[i]] = v_new[i], each
+ * row Hkv * D bf16.  Slots outside [0, pool_slots) are skipped.  Pointers
+ * must be 16-byte aligned. */
+int ra_store_kv(const int32_t* slots, const void* k_new, const void* v_new, int64_t n_tokens,
+                void* k_pool, void* v_pool, int64_t pool_slots, int32_t hkv, int32_t d,
+                hipStream_t stream);
+
+/* Extend attention (prefill of new tokens over a cached prefix; Appendix A.1
+ * defines prefill, section 3 the reuse of a prefix's KV cache).
+ *   q      [total_tokens, Hq, D] bf16, rows of request r at extend_start[r] ..
+ *   k_new, v_new [total_tokens, Hkv, D] bf16, the new tokens' K and V (same rows)
+ *   k_pool, v_pool [pool_slots, Hkv, D] bf16; prefix position j < P_r of
+ *          request r is read from slot req_to_token[req_pool_idx[r] *
+ *          rtt_stride + j]; req_to_token is int32 [rtt_rows, rtt_stride]
+ *   prefix_lens, extend_lens, extend_start, req_pool_idx: int32 [B]
+ *   max_extend_len: host upper bound of extend_lens (sizes the grid)
+ *   out    [sum E, Hq, D] bf16
+ * New token i of request r (position P_r + i) attends positions 0 .. P_r + i.
+ * Requires Hq % Hkv == 0, G = Hq / Hkv in {1, 2, 4, 8, 16}, D in {64, 128}.
+ * Device-side bounds: table rows, prefix lengths, token rows and slots are
+ * clamped into their arrays (out-of-range inputs give undefined values, never
+ * an out-of-bounds access). */
+int ra_extend_attention(const void* q, const void* k_new, const void* v_new, int64_t total_tokens,
+                        const void* k_pool, const void* v_pool, int64_t pool_slots,
+                        const int32_t* req_to_token, int64_t rtt_rows, int64_t rtt_stride,
+                        const int32_t* req_pool_idx, const int32_t* prefix_lens,
+                        const int32_t* extend_lens, const int32_t* extend_start, int32_t batch,
+                        int32_t max_extend_len, int32_t hq, int32_t hkv, int32_t d, float scale,
+                        void* out, hipStream_t stream);
+
+/* Decode attention: query r ([B, Hq, D] bf16) at position L_r - 1 over
+ * positions 0 .. L_r - 1 (its own K/V already stored), seq_lens = L_r >= 1.
+ * Long contexts are cut into KV chunks processed in parallel; each chunk
+ * writes a normalised partial output and its log-sum-exp to `workspace`, and
+ * a second pass merges them.  num_splits = 0 picks the chunking; otherwise the
+ * context is cut into at most num_splits chunks.  max_seq_len bounds seq_lens
+ * (0 means rtt_stride).  workspace must hold ra_decode_workspace_bytes(...)
+ * bytes for the same arguments (NULL allowed when that is 0).  Lengths above
+ * max_seq_len are clamped to it.  Same head, table and slot rules as extend;
+ * G = Hq / Hkv may be any value from 1 to 16. */
+size_t ra_decode_workspace_bytes(int32_t batch, int32_t hq, int32_t hkv, int32_t d,
+                                 int32_t max_seq_len, int32_t num_splits);
+int ra_decode_attention(const void* q, const void* k_pool, const void* v_pool, int64_t pool_slots,
+                        const int32_t* req_to_token, int64_t rtt_rows, int64_t rtt_stride,
+                        const int32_t* req_pool_idx,
+                        const int32_t* seq_lens, int32_t batch, int32_t max_seq_len, int32_t hq,
+                        int32_t hkv, int32_t d, float scale, int32_t num_splits, void* workspace,
+                        size_t workspace_bytes, void* out, hipStream_t stream);
+
+/* The chunk length (tokens) decode uses for these arguments. */
+int32_t ra_decode_chunk_len(int32_t batch, int32_t hkv, int32_t max_seq_len, int32_t num_splits);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* RADIXATTN_H */

@@ -1,0 +1,255 @@
+"""RadixAttention hot path for MI355X (gfx950): Python binding of libradixattn.
+
+Argument marshalling only.  Every step runs in the native library: the host
+radix cache in C++, attention and the KV scatter in HIP kernels.  Torch
+tensors provide device memory and the current HIP stream.  Importing this
+package fails if the native library has not been built (``build_lib.py``).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libradixattn.so")
+
+RA_OK, RA_EINVAL, RA_ENOMEM, RA_EHIP = 0, -1, -2, -3
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(f"{LIB_PATH} is missing: build it with `python {_HERE}/build_lib.py`")
+
+_lib = ctypes.CDLL(LIB_PATH)
+
+_i32p = ctypes.POINTER(ctypes.c_int32)
+_i64p = ctypes.POINTER(ctypes.c_int64)
+_vp = ctypes.c_void_p
+_i64 = ctypes.c_int64
+_i32 = ctypes.c_int32
+
+_SIGS = {
+    "ra_last_error": ([], ctypes.c_char_p),
+    "ra_cache_create": ([_i64, _vp, ctypes.POINTER(_vp)], ctypes.c_int),
+    "ra_cache_destroy": ([_vp], None),
+    "ra_match_prefix": ([_vp, _vp, _i64, _vp, _i64p, _i64p], ctypes.c_int),
+    "ra_inc_ref": ([_vp, _i64, _i64p], ctypes.c_int),
+    "ra_dec_ref": ([_vp, _i64, _i64p], ctypes.c_int),
+    "ra_alloc_slots": ([_vp, _i64, _vp], ctypes.c_int),
+    "ra_free_slots": ([_vp, _vp, _i64], ctypes.c_int),
+    "ra_insert": ([_vp, _vp, _vp, _i64, _i64p, _i64p], ctypes.c_int),
+    "ra_evict": ([_vp, _i64, _i64p], ctypes.c_int),
+    "ra_evictable_size": ([_vp], _i64),
+    "ra_available_size": ([_vp], _i64),
+    "ra_cached_tokens": ([_vp], _i64),
+    "ra_num_nodes": ([_vp], _i64),
+    "ra_snapshot": ([_vp, _vp, _i64, _i64p], ctypes.c_int),
+    "ra_store_kv": ([_vp, _vp, _vp, _i64, _vp, _vp, _i64, _i32, _i32, _vp], ctypes.c_int),
+    "ra_extend_attention": ([_vp, _vp, _vp, _i64, _vp, _vp, _i64, _vp, _i64, _i64, _vp, _vp, _vp, _vp,
+                             _i32, _i32, _i32, _i32, _i32, ctypes.c_float, _vp, _vp], ctypes.c_int),
+    "ra_decode_workspace_bytes": ([_i32, _i32, _i32, _i32, _i32, _i32], ctypes.c_size_t),
+    "ra_decode_chunk_len": ([_i32, _i32, _i32, _i32], _i32),
+    "ra_decode_attention": ([_vp, _vp, _vp, _i64, _vp, _i64, _i64, _vp, _vp, _i32, _i32, _i32, _i32, _i32,
+                             ctypes.c_float, _i32, _vp, ctypes.c_size_t, _vp, _vp], ctypes.c_int),
+}
+for _name, (_args, _res) in _SIGS.items():
+    _f = getattr(_lib, _name)
+    _f.argtypes = _args
+    _f.restype = _res
+
+EXPORTED = tuple(_SIGS)
+
+
+class RadixAttnError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"[{code}] {msg}")
+        self.code = code
+
+
+class OutOfSlots(RadixAttnError):
+    pass
+
+
+def _check(code: int) -> None:
+    if code != RA_OK:
+        msg = _lib.ra_last_error().decode()
+        raise (OutOfSlots if code == RA_ENOMEM else RadixAttnError)(code, msg)
+
+
+def _np_i32(a) -> np.ndarray:
+    return np.ascontiguousarray(a, dtype=np.int32)
+
+
+# ---------------------------------------------------------------------------
+# Host radix cache
+# ---------------------------------------------------------------------------
+
+class RadixCache:
+    """The native radix tree + slot pool (one handle, one scheduler thread)."""
+
+    def __init__(self, pool_slots: int, free_order=None):
+        h = _vp()
+        order = None if free_order is None else _np_i32(free_order)
+        if order is not None and order.shape[0] != pool_slots:
+            raise ValueError("free_order must have pool_slots entries")
+        _check(_lib.ra_cache_create(pool_slots, None if order is None else order.ctypes.data, ctypes.byref(h)))
+        self._h = h
+        self.pool_slots = pool_slots
+
+    def __del__(self):
+        h = getattr(self, "_h", None)
+        if h:
+            _lib.ra_cache_destroy(h)
+            self._h = None
+
+    def match_prefix(self, tokens):
+        t = _np_i32(tokens)
+        slots = np.empty(t.shape[0], dtype=np.int32)
+        n, node = _i64(), _i64()
+        _check(_lib.ra_match_prefix(self._h, t.ctypes.data, t.shape[0], slots.ctypes.data,
+                                    ctypes.byref(n), ctypes.byref(node)))
+        return node.value, n.value, slots[: n.value]
+
+    def inc_ref(self, node: int) -> int:
+        d = _i64()
+        _check(_lib.ra_inc_ref(self._h, node, ctypes.byref(d)))
+        return d.value
+
+    def dec_ref(self, node: int) -> int:
+        d = _i64()
+        _check(_lib.ra_dec_ref(self._h, node, ctypes.byref(d)))
+        return d.value
+
+    def alloc(self, n: int) -> np.ndarray:
+        out = np.empty(n, dtype=np.int32)
+        _check(_lib.ra_alloc_slots(self._h, n, out.ctypes.data))
+        return out
+
+    def free_slots(self, slots) -> None:
+        s = _np_i32(slots)
+        _check(_lib.ra_free_slots(self._h, s.ctypes.data, s.shape[0]))
+
+    def insert(self, tokens, slots):
+        t, s = _np_i32(tokens), _np_i32(slots)
+        if t.shape != s.shape:
+            raise ValueError("tokens and slots differ in length")
+        cached, node = _i64(), _i64()
+        _check(_lib.ra_insert(self._h, t.ctypes.data, s.ctypes.data, t.shape[0], ctypes.byref(cached),
+                              ctypes.byref(node)))
+        return cached.value, node.value
+
+    def evict(self, n_tokens: int) -> int:
+        f = _i64()
+        _check(_lib.ra_evict(self._h, n_tokens, ctypes.byref(f)))
+        return f.value
+
+    def evictable_size(self) -> int:
+        return _lib.ra_evictable_size(self._h)
+
+    def available_size(self) -> int:
+        return _lib.ra_available_size(self._h)
+
+    def cached_tokens(self) -> int:
+        return _lib.ra_cached_tokens(self._h)
+
+    def num_nodes(self) -> int:
+        return _lib.ra_num_nodes(self._h)
+
+    def snapshot(self) -> dict:
+        """Same canonical form as the oracle's RadixCache.snapshot()."""
+        n = _i64()
+        _check(_lib.ra_snapshot(self._h, None, 0, ctypes.byref(n)))
+        buf = np.empty(n.value, dtype=np.int64)
+        _check(_lib.ra_snapshot(self._h, buf.ctypes.data, n.value, ctypes.byref(n)))
+        clock, n_nodes, n_free = int(buf[0]), int(buf[1]), int(buf[2])
+        nodes, i = [], 3
+        for _ in range(n_nodes):
+            nid, parent, ref, stamp, ln = (int(x) for x in buf[i : i + 5])
+            i += 5
+            key = tuple(int(x) for x in buf[i : i + ln])
+            slots = tuple(int(x) for x in buf[i + ln : i + 2 * ln])
+            i += 2 * ln
+            nodes.append((nid, parent, ref, stamp, key, slots))
+        free = [int(x) for x in buf[i : i + n_free]]
+        return {"nodes": nodes, "free": free, "clock": clock}
+
+
+# ---------------------------------------------------------------------------
+# Device calls (torch tensors; the current stream unless one is given)
+# ---------------------------------------------------------------------------
+
+def _stream(stream):
+    import torch
+
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _dev(t, dtype=None, name="tensor"):
+    import torch
+
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise TypeError(f"{name} must be a CUDA (HIP) tensor")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def ra_store_kv(slots, k_new, v_new, k_pool, v_pool, stream=None) -> None:
+    import torch
+
+    n, hkv, d = k_new.shape
+    _check(_lib.ra_store_kv(_dev(slots, torch.int32, "slots"), _dev(k_new, torch.bfloat16, "k_new"),
+                            _dev(v_new, torch.bfloat16, "v_new"), n, _dev(k_pool, torch.bfloat16, "k_pool"),
+                            _dev(v_pool, torch.bfloat16, "v_pool"), k_pool.shape[0], hkv, d, _stream(stream)))
+
+
+def ra_extend_attention(q, k_new, v_new, k_pool, v_pool, req_to_token, req_pool_idx, prefix_lens, extend_lens,
+                        extend_start, max_extend_len: int, scale: float, out=None, stream=None):
+    import torch
+
+    total, hq, d = q.shape
+    hkv = k_new.shape[1]
+    if out is None:
+        out = torch.empty_like(q)
+    _check(_lib.ra_extend_attention(
+        _dev(q, torch.bfloat16, "q"), _dev(k_new, torch.bfloat16, "k_new"), _dev(v_new, torch.bfloat16, "v_new"),
+        total, _dev(k_pool, torch.bfloat16, "k_pool"), _dev(v_pool, torch.bfloat16, "v_pool"), k_pool.shape[0],
+        _dev(req_to_token, torch.int32, "req_to_token"), req_to_token.shape[0], req_to_token.shape[1],
+        _dev(req_pool_idx, torch.int32, "req_pool_idx"), _dev(prefix_lens, torch.int32, "prefix_lens"),
+        _dev(extend_lens, torch.int32, "extend_lens"), _dev(extend_start, torch.int32, "extend_start"),
+        prefix_lens.shape[0], int(max_extend_len), hq, hkv, d, float(scale), _dev(out, torch.bfloat16, "out"),
+        _stream(stream)))
+    return out
+
+
+def ra_decode_workspace_bytes(batch: int, hq: int, hkv: int, d: int, max_seq_len: int, num_splits: int = 0) -> int:
+    return int(_lib.ra_decode_workspace_bytes(batch, hq, hkv, d, max_seq_len, num_splits))
+
+
+def ra_decode_chunk_len(batch: int, hkv: int, max_seq_len: int, num_splits: int = 0) -> int:
+    return int(_lib.ra_decode_chunk_len(batch, hkv, max_seq_len, num_splits))
+
+
+def ra_decode_attention(q, k_pool, v_pool, req_to_token, req_pool_idx, seq_lens, max_seq_len: int, scale: float,
+                        num_splits: int = 0, workspace=None, out=None, stream=None):
+    import torch
+
+    b, hq, d = q.shape
+    hkv = k_pool.shape[1]
+    need = ra_decode_workspace_bytes(b, hq, hkv, d, max_seq_len, num_splits)
+    if workspace is None and need:
+        workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
+    if out is None:
+        out = torch.empty_like(q)
+    ws_ptr = _dev(workspace, None, "workspace") if workspace is not None else None
+    ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    _check(_lib.ra_decode_attention(
+        _dev(q, torch.bfloat16, "q"), _dev(k_pool, torch.bfloat16, "k_pool"), _dev(v_pool, torch.bfloat16, "v_pool"),
+        k_pool.shape[0], _dev(req_to_token, torch.int32, "req_to_token"), req_to_token.shape[0],
+        req_to_token.shape[1], _dev(req_pool_idx, torch.int32, "req_pool_idx"),
+        _dev(seq_lens, torch.int32, "seq_lens"), b, int(max_seq_len), hq, hkv, d, float(scale), int(num_splits),
+        ws_ptr, ws_bytes, _dev(out, torch.bfloat16, "out"), _stream(stream)))
+    return out

@@ -1,0 +1,380 @@
+// Host radix cache: radix tree over token ids, reference counters, LRU leaf
+// eviction and the shared FIFO slot pool (section 3 of the SGLang paper and
+// Algorithm 1).  Semantics, including where the paper is silent:
+//  * match_prefix and insert each advance a logical clock once and stamp
+//    every node they walk ("used" for LRU);
+//  * eviction takes the unreferenced leaf with the smallest (stamp, id),
+//    frees whole leaves, and re-examines a parent that becomes a leaf;
+//  * a match ending inside an edge splits it; a split keeps the old id for
+//    the lower part, gives the upper part the next id, the old counter and
+//    the old stamp;
+//  * a reference lock covers the whole root-to-node path;
+//  * insert keeps cached slots and frees caller slots that differ from them;
+//  * the pool is a FIFO queue with a caller-given initial order.
+//
+// Data layout for large trees (hundreds of thousands of operations over
+// millions of tokens): nodes live in a vector indexed by id; the child edge
+// index is one hash map keyed by (parent id, first token); the evictable
+// leaves are an ordered set keyed by (stamp, id), kept current on every
+// change, so eviction never scans the tree.
+#include <algorithm>
+#include <cstdint>
+#include <cstring>
+#include <set>
+#include <string>
+#include <unordered_map>
+#include <vector>
+
+#include "radixattn.h"
+#include "ra_error.h"
+
+namespace {
+
+struct Node {
+  int64_t parent = -1;
+  std::vector<int32_t> key;
+  std::vector<int32_t> slots;
+  int64_t ref = 0;
+  uint64_t stamp = 0;
+  int64_t n_children = 0;
+  bool alive = false;
+  bool in_lru = false;   // present in the evictable-leaf set
+  uint64_t lru_stamp = 0;  // stamp it was filed under
+};
+
+inline uint64_t edge_key(int64_t parent, int32_t tok) {
+  return (static_cast<uint64_t>(parent) << 32) ^ static_cast<uint32_t>(tok);
+}
+
+}  // namespace
+
+struct ra_cache {
+  int64_t pool_slots = 0;
+  // FIFO free queue as a ring buffer of capacity pool_slots
+  std::vector<int32_t> ring;
+  int64_t head = 0, count = 0;
+  std::vector<uint8_t> is_free;
+
+  std::vector<Node> nodes;
+  std::unordered_map<uint64_t, int64_t> children;  // (parent, first token) -> child
+  std::set<std::pair<uint64_t, int64_t>> lru;      // evictable leaves
+  uint64_t clock = 0;
+  int64_t live = 1;
+  int64_t evictable = 0;  // tokens in unreferenced live nodes
+  int64_t cached = 0;     // tokens in live nodes
+
+  bool evictable_leaf(int64_t id) const {
+    const Node& n = nodes[id];
+    return id != 0 && n.alive && n.ref == 0 && n.n_children == 0;
+  }
+  void refresh(int64_t id) {
+    Node& n = nodes[id];
+    bool want = evictable_leaf(id);
+    if (n.in_lru && (!want || n.lru_stamp != n.stamp)) {
+      lru.erase({n.lru_stamp, id});
+      n.in_lru = false;
+    }
+    if (want && !n.in_lru) {
+      lru.insert({n.stamp, id});
+      n.in_lru = true;
+      n.lru_stamp = n.stamp;
+    }
+  }
+
+  // ---- pool ----
+  void push_free(int32_t s) {
+    ring[(head + count) % pool_slots] = s;
+    ++count;
+    is_free[s] = 1;
+  }
+  int32_t pop_free() {
+    int32_t s = ring[head];
+    head = (head + 1) % pool_slots;
+    --count;
+    is_free[s] = 0;
+    return s;
+  }
+
+  // ---- tree ----
+  // Appends a node.  key and slots are taken by value: callers may pass
+  // views into another node, which the vector growth below would invalidate.
+  int64_t new_node(int64_t parent, std::vector<int32_t> key, std::vector<int32_t> slots,
+                   int64_t ref, uint64_t stamp) {
+    int64_t id = static_cast<int64_t>(nodes.size());
+    nodes.emplace_back();
+    Node& n = nodes.back();
+    n.parent = parent;
+    n.key = std::move(key);
+    n.slots = std::move(slots);
+    n.ref = ref;
+    n.stamp = stamp;
+    n.alive = true;
+    ++live;
+    return id;
+  }
+
+  // Splits node x after c tokens; returns the new upper node.
+  int64_t split(int64_t x, int64_t c) {
+    int64_t par = nodes[x].parent;
+    int32_t first = nodes[x].key[0];
+    int64_t y = new_node(par, std::vector<int32_t>(nodes[x].key.begin(), nodes[x].key.begin() + c),
+                         std::vector<int32_t>(nodes[x].slots.begin(), nodes[x].slots.begin() + c),
+                         nodes[x].ref, nodes[x].stamp);
+    Node& X = nodes[x];
+    Node& Y = nodes[y];
+    X.key.erase(X.key.begin(), X.key.begin() + c);
+    X.slots.erase(X.slots.begin(), X.slots.begin() + c);
+    X.parent = y;
+    Y.n_children = 1;
+    children[edge_key(par, first)] = y;
+    children[edge_key(y, X.key[0])] = x;
+    refresh(x);
+    refresh(y);
+    return y;
+  }
+
+  // Walks tokens from the root; calls visit(node, pos) on every matched node.
+  template <class F>
+  int64_t walk(const int32_t* tok, int64_t n, int64_t* out_pos, F&& visit) {
+    ++clock;
+    int64_t node = 0, pos = 0;
+    while (pos < n) {
+      auto it = children.find(edge_key(node, tok[pos]));
+      if (it == children.end()) break;
+      int64_t ch = it->second;
+      const std::vector<int32_t>& key = nodes[ch].key;
+      int64_t lim = std::min<int64_t>(static_cast<int64_t>(key.size()), n - pos);
+      int64_t c = 0;
+      while (c < lim && key[c] == tok[pos + c]) ++c;
+      if (c < static_cast<int64_t>(key.size())) ch = split(ch, c);
+      nodes[ch].stamp = clock;
+      refresh(ch);
+      visit(ch, pos);
+      pos += c;
+      node = ch;
+    }
+    *out_pos = pos;
+    return node;
+  }
+};
+
+extern "C" {
+
+int ra_cache_create(int64_t pool_slots, const int32_t* order, ra_cache** out) {
+  if (!out) return ra_fail(RA_EINVAL, "ra_cache_create: out is NULL");
+  if (pool_slots < 0 || pool_slots > INT32_MAX)
+    return ra_fail(RA_EINVAL, "ra_cache_create: pool_slots out of range");
+  ra_cache* c = new ra_cache();
+  c->pool_slots = pool_slots;
+  c->ring.resize(static_cast<size_t>(pool_slots));
+  c->is_free.assign(static_cast<size_t>(pool_slots), 0);
+  for (int64_t i = 0; i < pool_slots; ++i) {
+    int32_t s = order ? order[i] : static_cast<int32_t>(i);
+    if (s < 0 || s >= pool_slots || c->is_free[s]) {
+      delete c;
+      return ra_fail(RA_EINVAL, "ra_cache_create: initial order is not a permutation");
+    }
+    c->push_free(s);
+  }
+  c->nodes.emplace_back();  // root
+  c->nodes[0].alive = true;
+  *out = c;
+  return ra_ok();
+}
+
+void ra_cache_destroy(ra_cache* c) { delete c; }
+
+int ra_match_prefix(ra_cache* c, const int32_t* tokens, int64_t n, int32_t* out_slots,
+                    int64_t* out_len, int64_t* out_node) {
+  if (!c || n < 0 || (n > 0 && !tokens)) return ra_fail(RA_EINVAL, "ra_match_prefix: bad argument");
+  int64_t pos = 0;
+  int64_t node = c->walk(tokens, n, &pos, [&](int64_t ch, int64_t p) {
+    if (out_slots) {
+      const auto& s = c->nodes[ch].slots;
+      std::memcpy(out_slots + p, s.data(), s.size() * sizeof(int32_t));
+    }
+  });
+  if (out_len) *out_len = pos;
+  if (out_node) *out_node = node;
+  return ra_ok();
+}
+
+static bool valid_node(const ra_cache* c, int64_t node) {
+  return node >= 0 && node < static_cast<int64_t>(c->nodes.size()) && c->nodes[node].alive;
+}
+
+int ra_inc_ref(ra_cache* c, int64_t node, int64_t* out_delta) {
+  if (!c || !valid_node(c, node)) return ra_fail(RA_EINVAL, "ra_inc_ref: unknown node");
+  int64_t delta = 0;
+  for (int64_t x = node; x != 0; x = c->nodes[x].parent) {
+    Node& n = c->nodes[x];
+    if (n.ref == 0) {
+      delta -= static_cast<int64_t>(n.key.size());
+    }
+    ++n.ref;
+    c->refresh(x);
+  }
+  c->evictable += delta;
+  if (out_delta) *out_delta = delta;
+  return ra_ok();
+}
+
+int ra_dec_ref(ra_cache* c, int64_t node, int64_t* out_delta) {
+  if (!c || !valid_node(c, node)) return ra_fail(RA_EINVAL, "ra_dec_ref: unknown node");
+  for (int64_t x = node; x != 0; x = c->nodes[x].parent)
+    if (c->nodes[x].ref == 0) return ra_fail(RA_EINVAL, "ra_dec_ref: reference counter underflow");
+  int64_t delta = 0;
+  for (int64_t x = node; x != 0; x = c->nodes[x].parent) {
+    Node& n = c->nodes[x];
+    if (--n.ref == 0) delta += static_cast<int64_t>(n.key.size());
+    c->refresh(x);
+  }
+  c->evictable += delta;
+  if (out_delta) *out_delta = delta;
+  return ra_ok();
+}
+
+int ra_alloc_slots(ra_cache* c, int64_t n, int32_t* out_slots) {
+  if (!c || n < 0 || (n > 0 && !out_slots)) return ra_fail(RA_EINVAL, "ra_alloc_slots: bad argument");
+  if (n > c->count) return ra_fail(RA_ENOMEM, "ra_alloc_slots: not enough free slots");
+  for (int64_t i = 0; i < n; ++i) out_slots[i] = c->pop_free();
+  return ra_ok();
+}
+
+static int check_freeable(ra_cache* c, const int32_t* slots, int64_t n, const char* who) {
+  // every slot in range, currently allocated, and not repeated
+  std::vector<int32_t> seen;
+  for (int64_t i = 0; i < n; ++i) {
+    int32_t s = slots[i];
+    if (s < 0 || s >= c->pool_slots || c->is_free[s])
+      return ra_fail(RA_EINVAL, std::string(who) + ": slot out of range or already free");
+  }
+  seen.assign(slots, slots + n);
+  std::sort(seen.begin(), seen.end());
+  if (std::adjacent_find(seen.begin(), seen.end()) != seen.end())
+    return ra_fail(RA_EINVAL, std::string(who) + ": repeated slot");
+  return RA_OK;
+}
+
+int ra_free_slots(ra_cache* c, const int32_t* slots, int64_t n) {
+  if (!c || n < 0 || (n > 0 && !slots)) return ra_fail(RA_EINVAL, "ra_free_slots: bad argument");
+  int st = check_freeable(c, slots, n, "ra_free_slots");
+  if (st != RA_OK) return st;
+  for (int64_t i = 0; i < n; ++i) c->push_free(slots[i]);
+  return ra_ok();
+}
+
+int ra_insert(ra_cache* c, const int32_t* tokens, const int32_t* slots, int64_t n,
+              int64_t* out_cached, int64_t* out_node) {
+  if (!c || n < 0 || (n > 0 && (!tokens || !slots))) return ra_fail(RA_EINVAL, "ra_insert: bad argument");
+  // Validate duplicates before changing anything: walk read-only first.
+  {
+    int64_t node = 0, pos = 0;
+    std::vector<int32_t> dup;
+    while (pos < n) {
+      auto it = c->children.find(edge_key(node, tokens[pos]));
+      if (it == c->children.end()) break;
+      const Node& ch = c->nodes[it->second];
+      int64_t lim = std::min<int64_t>(static_cast<int64_t>(ch.key.size()), n - pos);
+      int64_t k = 0;
+      while (k < lim && ch.key[k] == tokens[pos + k]) {
+        if (slots[pos + k] != ch.slots[k]) dup.push_back(slots[pos + k]);
+        ++k;
+      }
+      pos += k;
+      if (k < static_cast<int64_t>(ch.key.size())) break;
+      node = it->second;
+    }
+    if (!dup.empty()) {
+      int st = check_freeable(c, dup.data(), static_cast<int64_t>(dup.size()), "ra_insert");
+      if (st != RA_OK) return st;
+    }
+    // slots that will enter the tree must be allocated pool slots
+    for (int64_t i = pos; i < n; ++i)
+      if (slots[i] < 0 || slots[i] >= c->pool_slots || c->is_free[slots[i]])
+        return ra_fail(RA_EINVAL, "ra_insert: new slot out of range or free");
+  }
+  std::vector<int32_t> dup;
+  int64_t pos = 0;
+  int64_t node = c->walk(tokens, n, &pos, [&](int64_t ch, int64_t p) {
+    const auto& s = c->nodes[ch].slots;
+    for (size_t i = 0; i < s.size(); ++i)
+      if (slots[p + i] != s[i]) dup.push_back(slots[p + i]);
+  });
+  for (int32_t s : dup) c->push_free(s);
+  int64_t cached = pos;
+  if (pos < n) {
+    int64_t leaf = c->new_node(node, std::vector<int32_t>(tokens + pos, tokens + n),
+                               std::vector<int32_t>(slots + pos, slots + n), 0, c->clock);
+    c->children[edge_key(node, tokens[pos])] = leaf;
+    c->nodes[node].n_children += 1;
+    c->evictable += n - pos;
+    c->cached += n - pos;
+    c->refresh(node);
+    c->refresh(leaf);
+    node = leaf;
+  }
+  if (out_cached) *out_cached = cached;
+  if (out_node) *out_node = node;
+  return ra_ok();
+}
+
+int ra_evict(ra_cache* c, int64_t n_tokens, int64_t* out_freed) {
+  if (!c) return ra_fail(RA_EINVAL, "ra_evict: cache is NULL");
+  int64_t freed = 0;
+  while (freed < n_tokens && !c->lru.empty()) {
+    int64_t x = c->lru.begin()->second;
+    c->lru.erase(c->lru.begin());
+    Node& n = c->nodes[x];
+    n.in_lru = false;
+    for (int32_t s : n.slots) c->push_free(s);
+    int64_t len = static_cast<int64_t>(n.key.size());
+    freed += len;
+    c->evictable -= len;
+    c->cached -= len;
+    c->children.erase(edge_key(n.parent, n.key[0]));
+    int64_t par = n.parent;
+    n.alive = false;
+    std::vector<int32_t>().swap(n.key);
+    std::vector<int32_t>().swap(n.slots);
+    --c->live;
+    c->nodes[par].n_children -= 1;
+    c->refresh(par);
+  }
+  if (out_freed) *out_freed = freed;
+  return ra_ok();
+}
+
+int64_t ra_evictable_size(const ra_cache* c) { return c ? c->evictable : 0; }
+int64_t ra_available_size(const ra_cache* c) { return c ? c->count : 0; }
+int64_t ra_cached_tokens(const ra_cache* c) { return c ? c->cached : 0; }
+int64_t ra_num_nodes(const ra_cache* c) { return c ? c->live : 0; }
+
+int ra_snapshot(const ra_cache* c, int64_t* buf, int64_t cap, int64_t* out_len) {
+  if (!c) return ra_fail(RA_EINVAL, "ra_snapshot: cache is NULL");
+  int64_t need = 3 + c->count;
+  for (const Node& n : c->nodes)
+    if (n.alive) need += 5 + 2 * static_cast<int64_t>(n.key.size());
+  if (out_len) *out_len = need;
+  if (!buf) return ra_ok();
+  if (cap < need) return ra_fail(RA_EINVAL, "ra_snapshot: buffer too small");
+  int64_t* w = buf;
+  *w++ = static_cast<int64_t>(c->clock);
+  *w++ = c->live;
+  *w++ = c->count;
+  for (size_t id = 0; id < c->nodes.size(); ++id) {
+    const Node& n = c->nodes[id];
+    if (!n.alive) continue;
+    *w++ = static_cast<int64_t>(id);
+    *w++ = n.parent;
+    *w++ = n.ref;
+    *w++ = static_cast<int64_t>(n.stamp);
+    *w++ = static_cast<int64_t>(n.key.size());
+    for (int32_t t : n.key) *w++ = t;
+    for (int32_t s : n.slots) *w++ = s;
+  }
+  for (int64_t i = 0; i < c->count; ++i) *w++ = c->ring[(c->head + i) % c->pool_slots];
+  return ra_ok();
+}
+
+}  // extern "C"

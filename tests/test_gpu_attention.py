@@ -1,0 +1,198 @@
+"""GPU parity: the HIP path (through the C ABI) against the float64 oracle.
+
+Every case prints its name, seed and shapes before touching the GPU.  Full-size
+workloads are compared on sampled requests / rows the oracle recomputes one by
+one; the small ones in full.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import attention as oa
+from workload import contentgen as cg
+from workload import scenarios as S
+
+pytestmark = pytest.mark.gpu
+
+if not torch.cuda.is_available():  # pragma: no cover - CPU-only container
+    pytest.skip("no GPU", allow_module_level=True)
+
+from tests.harness import ScenarioRun, assert_close, errors, log  # noqa: E402
+
+
+def _bf(t):
+    return t.float().cpu().numpy()
+
+
+def run_phase(run, idx, num_splits=0):
+    inp = run.prepare(idx)
+    run.store(inp)
+    oe = run.extend(inp)
+    od = run.decode(inp, num_splits=num_splits)
+    torch.cuda.synchronize()
+    return inp, oe, od
+
+
+def check_decode(run, inp, od, sample=None, what=""):
+    sc = run.sc
+    idx = range(inp.n_dec) if sample is None else sample
+    got = _bf(od)
+    worst = None
+    for i in idx:
+        toks, L = inp.dec_meta[i]
+        ref = oa.decode_reference(toks, L, sc.seed, sc.hq, sc.hkv, sc.d, sc.scale, sc.q_scale_pow2)
+        er = assert_close(got[i], ref, f"{what} decode req {i} L={L}")
+        worst = er if worst is None or er["max"] > worst["max"] else worst
+    return worst
+
+
+def check_extend(run, inp, oe, sample=None, rows_per_req=None, what="", seed=0):
+    sc = run.sc
+    rng = np.random.default_rng(seed)
+    idx = range(inp.n_ext) if sample is None else sample
+    got = _bf(oe)
+    worst = None
+    for i in idx:
+        toks, p, e, start = inp.ext_meta[i]
+        rows = np.arange(e) if rows_per_req is None or rows_per_req >= e else np.unique(
+            np.concatenate([[0, e - 1], rng.choice(e, rows_per_req, replace=False)]))
+        ref = oa.extend_reference(toks, p, e, sc.seed, sc.hq, sc.hkv, sc.d, sc.scale, sc.q_scale_pow2, rows=rows)
+        er = assert_close(got[start + rows], ref, f"{what} extend req {i} P={p} E={e}")
+        worst = er if worst is None or er["max"] > worst["max"] else worst
+    return worst
+
+
+# ----------------------------------------------------------- generator -----
+
+def test_gpu_generator_bit_exact():
+    log("case: generator bit-exact, 3000 positions x 1024")
+    h = cg.prefix_hashes(np.arange(3000, dtype=np.int32) % 977, 11)
+    out = torch.empty((3000, 8, 128), dtype=torch.bfloat16, device="cuda")
+    from workload import gpu_gen
+    gpu_gen.fill(out, h, cg.STREAM_V)
+    got = out.view(torch.int16).cpu().numpy().view(np.uint16).reshape(3000, -1)
+    assert np.array_equal(got, cg.values_bf16_bits(h, cg.STREAM_V, 1024))
+    rows = np.random.default_rng(0).permutation(3000)[:500]
+    out2 = torch.zeros((3000, 8, 128), dtype=torch.bfloat16, device="cuda")
+    gpu_gen.fill(out2, h[:500], cg.STREAM_K, rows=rows, scale_pow2=2)
+    got2 = out2.float().cpu().numpy()[rows]
+    assert np.array_equal(got2, cg.values(h[:500], cg.STREAM_K, 8, 128, 2))
+
+
+# ------------------------------------------------------------ store_kv -----
+
+@pytest.mark.parametrize("hkv,d", [(8, 64), (8, 128), (2, 128)])
+def test_store_kv_bit_exact(hkv, d):
+    import paper_2312_07104_amd as pa
+    log(f"case: store_kv hkv={hkv} d={d}")
+    rng = np.random.default_rng(hkv * d)
+    S_ = 5000
+    n = 777
+    slots = rng.choice(S_, n, replace=False).astype(np.int32)
+    slots[5] = -1          # skipped
+    slots[9] = S_ + 3      # skipped
+    kp = torch.zeros((S_, hkv, d), dtype=torch.bfloat16, device="cuda")
+    vp = torch.zeros_like(kp)
+    kn = torch.randn((n, hkv, d), device="cuda").bfloat16()
+    vn = torch.randn((n, hkv, d), device="cuda").bfloat16()
+    pa.ra_store_kv(torch.from_numpy(slots).cuda(), kn, vn, kp, vp)
+    torch.cuda.synchronize()
+    ok = (slots >= 0) & (slots < S_)
+    s = torch.from_numpy(slots[ok]).long().cuda()
+    assert torch.equal(kp[s], kn[torch.from_numpy(ok).cuda()])
+    assert torch.equal(vp[s], vn[torch.from_numpy(ok).cuda()])
+    untouched = np.ones(S_, bool)
+    untouched[slots[ok]] = False
+    assert int(kp[torch.from_numpy(untouched).cuda()].abs().sum()) == 0
+
+
+# --------------------------------------------------------- full configs -----
+
+def test_decode_tiny_full():
+    sc = S.cfg1_decode_tiny()
+    log(f"case: decode_tiny seed={sc.seed}")
+    run = ScenarioRun(sc)
+    inp, _, od = run_phase(run, 0)
+    er = check_decode(run, inp, od, what="decode_tiny")
+    log("decode_tiny worst", er)
+
+
+@pytest.fixture(scope="module")
+def fewshot():
+    sc = S.cfg2_extend_fewshot()
+    log(f"case: extend_fewshot seed={sc.seed}")
+    run = ScenarioRun(sc)
+    inp, oe, _ = run_phase(run, 0)
+    return run, inp, oe
+
+
+def test_extend_fewshot_sampled(fewshot):
+    run, inp, oe = fewshot
+    er = check_extend(run, inp, oe, sample=[0, 17, 63], what="extend_fewshot")
+    log("extend_fewshot worst", er)
+
+
+@pytest.fixture(scope="module")
+def chat():
+    sc = S.cfg3_decode_chat()
+    log(f"case: decode_chat seed={sc.seed}")
+    run = ScenarioRun(sc)
+    inp, _, od = run_phase(run, 0)
+    return run, inp, od
+
+
+def test_decode_chat_sampled(chat):
+    run, inp, od = chat
+    lens = np.array([l for _, l in inp.dec_meta])
+    sample = sorted({int(lens.argmin()), int(lens.argmax()), 0, 100, 255})
+    er = check_decode(run, inp, od, sample=sample, what="decode_chat")
+    log("decode_chat worst", er)
+
+
+def test_decode_splits_agree(chat):
+    run, inp, od = chat
+    sample = [3, 77]
+    for ns in (1, 2, 7):
+        log(f"case: decode_chat num_splits={ns}")
+        o2 = run.decode(inp, num_splits=ns)
+        torch.cuda.synchronize()
+        check_decode(run, inp, o2, sample=sample, what=f"splits={ns}")
+        assert errors(_bf(o2), _bf(od))["max"] <= 2e-2
+
+
+def test_branching_two_phases():
+    sc = S.cfg4_branching()
+    log(f"case: branching seed={sc.seed}")
+    run = ScenarioRun(sc)
+    inp, oe, _ = run_phase(run, 0)
+    er = check_extend(run, inp, oe, sample=[0, 31, 63], rows_per_req=24, what="branching/extend")
+    log("branching extend worst", er)
+    run.finish(0, inp)
+    inp2, _, od = run_phase(run, 1)
+    # decode contexts hit the pool written by store_kv in phase 1
+    assert all(m == c for m, c in zip(inp2.plan.matched, inp2.plan.ctx_lens))
+    er = check_decode(run, inp2, od, sample=[0, 1, 40, 63], what="branching/decode")
+    log("branching decode worst", er)
+
+
+def test_mixed_full_size_sampled():
+    sc = S.cfg5_mixed()
+    log(f"case: mixed seed={sc.seed} (history replay on host)")
+    run = ScenarioRun(sc)
+    log(f"history ops={run.history_ops} in {run.history_seconds:.2f}s")
+    inp, oe, od = run_phase(run, 0)
+    er = check_extend(run, inp, oe, sample=[0, 13, 31], rows_per_req=16, what="mixed/extend")
+    log("mixed extend worst", er)
+    lens = np.array([l for _, l in inp.dec_meta])
+    er = check_decode(run, inp, od, sample=sorted({int(lens.argmax()), int(lens.argmin()), 5, 300}),
+                      what="mixed/decode")
+    log("mixed decode worst", er)
+
+
+def test_mixed_small_full():
+    sc = S.cfg5_mixed_small()
+    log(f"case: mixed_small seed={sc.seed}")
+    run = ScenarioRun(sc)
+    inp, oe, od = run_phase(run, 0)
+    check_extend(run, inp, oe, what="mixed_small/extend")
+    check_decode(run, inp, od, what="mixed_small/decode")

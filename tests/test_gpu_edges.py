@@ -1,0 +1,217 @@
+"""GPU edge cases: degenerate lengths, ragged tiles, chunk boundaries, needles,
+sharpened scores, slot-permutation invariance, reuse versus recomputation."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import attention as oa
+from workload import contentgen as cg
+from workload import scenarios as S
+
+pytestmark = pytest.mark.gpu
+
+if not torch.cuda.is_available():  # pragma: no cover
+    pytest.skip("no GPU", allow_module_level=True)
+
+import paper_2312_07104_amd as pa  # noqa: E402
+from tests.harness import ScenarioRun, assert_close, log  # noqa: E402
+from workload import gpu_gen  # noqa: E402
+
+
+def _bf(t):
+    return t.float().cpu().numpy()
+
+
+def _scenario(name, hq, hkv, d, pool, extend=(), decode=(), seed=77, q_pow2=0):
+    ext = []
+    for i, (p, e) in enumerate(extend):
+        ext.append(S.ExtendReq(cg.run_tokens(seed * 1000 + i, p + e, S.VOCAB), p, e))
+    dec = []
+    for i, l in enumerate(decode):
+        dec.append(S.DecodeReq(cg.run_tokens(seed * 1000 + 500 + i, l, S.VOCAB), l))
+    sc = S.Scenario(name, seed, hq, hkv, d, pool, 0, lambda i: None, [S.Phase(extend=ext, decode=dec)])
+    sc.q_scale_pow2 = q_pow2
+    return sc
+
+
+def _run(sc, num_splits=0):
+    run = ScenarioRun(sc)
+    inp = run.prepare(0)
+    run.store(inp)
+    oe = run.extend(inp)
+    od = run.decode(inp, num_splits=num_splits)
+    torch.cuda.synchronize()
+    return run, inp, oe, od
+
+
+def _check_all(run, inp, oe, od, what):
+    sc = run.sc
+    if oe is not None:
+        got = _bf(oe)
+        for toks, p, e, start in inp.ext_meta:
+            if e == 0:
+                continue
+            ref = oa.extend_reference(toks, p, e, sc.seed, sc.hq, sc.hkv, sc.d, sc.scale, sc.q_scale_pow2)
+            assert_close(got[start:start + e], ref, f"{what} extend P={p} E={e}")
+    if od is not None:
+        got = _bf(od)
+        for i, (toks, l) in enumerate(inp.dec_meta):
+            ref = oa.decode_reference(toks, l, sc.seed, sc.hq, sc.hkv, sc.d, sc.scale, sc.q_scale_pow2)
+            assert_close(got[i], ref, f"{what} decode L={l}")
+
+
+@pytest.mark.parametrize("hq,hkv,d", [(8, 8, 64), (32, 8, 128), (16, 1, 128), (6, 2, 64)])
+def test_single_key_returns_v_exactly(hq, hkv, d):
+    log(f"case: single key hq={hq} hkv={hkv} d={d}")
+    ext = [(0, 1)] if (hq // hkv) in (1, 2, 4, 8, 16) else []
+    sc = _scenario("single", hq, hkv, d, 64, extend=ext, decode=[1, 1])
+    run, inp, oe, od = _run(sc)
+    v = run.v_pool.float().cpu().numpy()
+    for i, (toks, l) in enumerate(inp.dec_meta):
+        slot = inp.plan.rows[inp.n_ext + i][0]
+        for h in range(hq):
+            assert np.array_equal(_bf(od)[i, h], v[slot, h // (hq // hkv)])
+    if oe is not None:
+        slot = inp.plan.rows[0][0]
+        for h in range(hq):
+            assert np.array_equal(_bf(oe)[0, h], v[slot, h // (hq // hkv)])
+
+
+@pytest.mark.parametrize("hq,hkv,d", [(8, 8, 64), (32, 8, 128), (64, 8, 128), (16, 1, 64), (32, 2, 128)])
+def test_ragged_extend_tiles(hq, hkv, d):
+    log(f"case: ragged extend hq={hq} hkv={hkv} d={d}")
+    ext = [(0, 1), (5, 130), (64, 63), (63, 65), (0, 200), (130, 7), (1, 0), (257, 129)]
+    sc = _scenario("ragged", hq, hkv, d, 4096, extend=ext, seed=hq + d)
+    run, inp, oe, od = _run(sc)
+    _check_all(run, inp, oe, od, "ragged")
+
+
+@pytest.mark.parametrize("num_splits", [0, 1, 3, 16])
+def test_decode_boundaries(num_splits):
+    lens = [1, 2, 31, 32, 33, 63, 64, 65, 255, 256, 257, 511, 512, 513, 1000, 2049]
+    log(f"case: decode boundaries num_splits={num_splits}")
+    sc = _scenario("bounds", 32, 8, 128, 16384, decode=lens, seed=5)
+    run, inp, oe, od = _run(sc, num_splits=num_splits)
+    _check_all(run, inp, oe, od, f"bounds/splits={num_splits}")
+
+
+@pytest.mark.parametrize("q_pow2", [2, 3])
+def test_sharpened_scores(q_pow2):
+    """Q ~ N(0, 16 or 64): softmax concentrates on few keys, so any wrong,
+    dropped or duplicated key moves the output by O(1)."""
+    log(f"case: sharpened q_pow2={q_pow2}")
+    sc = _scenario("sharp", 32, 8, 128, 8192, extend=[(300, 77), (0, 129)], decode=[700, 64, 1537], seed=9,
+                   q_pow2=q_pow2)
+    run, inp, oe, od = _run(sc)
+    _check_all(run, inp, oe, od, "sharp")
+
+
+def test_decode_needles():
+    """A key equal to 8x one head's query dominates that head's softmax: the
+    output must be that position's V, at tile and chunk boundaries."""
+    L = 1100
+    sc = _scenario("needle", 16, 4, 128, 4096, decode=[L], seed=21)
+    run = ScenarioRun(sc)
+    inp = run.prepare(0)
+    run.store(inp)
+    torch.cuda.synchronize()
+    toks, _ = inp.dec_meta[0]
+    row = inp.plan.rows[0]
+    chunk = pa.ra_decode_chunk_len(1, 4, L, 3)
+    k_ref, v_ref, h = oa.request_kv(toks, sc.seed, sc.hkv, sc.d)
+    q = cg.values(h[L - 1:L], cg.STREAM_Q, sc.hq, sc.d)[0]
+    for j in (0, 31, 32, chunk - 1, chunk, L - 2, L - 1):
+        for head in (0, 7, 13):
+            log(f"case: needle pos={j} head={head}")
+            g = head // 4
+            kk = k_ref.copy()
+            kk[j, g] = cg.bf16_bits_to_f32(cg.f32_to_bf16_bits_rne(q[head] * 8))
+            saved = run.k_pool[row[j], g].clone()
+            run.k_pool[row[j], g] = torch.from_numpy(kk[j, g]).to(torch.bfloat16).cuda()
+            out = run.decode(inp, num_splits=3)
+            torch.cuda.synchronize()
+            run.k_pool[row[j], g] = saved
+            qq = cg.values(h[L - 1:L], cg.STREAM_Q, sc.hq, sc.d)
+            ref = oa.attend(qq, kk, v_ref, np.array([L - 1]), sc.scale)[0]
+            got = _bf(out)[0]
+            assert_close(got, ref, f"needle {j}/{head}")
+            assert np.abs(got[head] - v_ref[j, g]).max() < 0.05
+
+
+def test_slot_permutation_is_bit_exact():
+    sc = S.cfg5_mixed_small()
+    log(f"case: slot permutation seed={sc.seed}")
+    run = ScenarioRun(sc)
+    inp = run.prepare(0)
+    run.store(inp)
+    oe = run.extend(inp)
+    od = run.decode(inp)
+    torch.cuda.synchronize()
+    perm = torch.from_numpy(np.random.default_rng(3).permutation(sc.pool_slots)).long().cuda()
+    k2 = torch.empty_like(run.k_pool)
+    v2 = torch.empty_like(run.v_pool)
+    k2[perm] = run.k_pool
+    v2[perm] = run.v_pool
+    t = inp.table.long()
+    table2 = torch.where(t >= 0, perm[t.clamp(min=0)], t).int().contiguous()
+    run.k_pool, run.v_pool = k2, v2
+    inp.table = table2
+    oe2 = run.extend(inp)
+    od2 = run.decode(inp)
+    torch.cuda.synchronize()
+    assert torch.equal(oe, oe2) and torch.equal(od, od2)
+
+
+@pytest.mark.parametrize("hq,hkv,p,e", [(32, 32, 2048, 128), (32, 8, 700, 90), (64, 8, 1500, 600)])
+def test_reused_prefix_equals_recompute(hq, hkv, p, e):
+    """Extend over a cached prefix read through the table equals extend of the
+    whole sequence as new tokens (prefix_len = 0), within tolerance."""
+    log(f"case: reuse vs recompute hq={hq} hkv={hkv} P={p} E={e}")
+    d, n = 128, p + e
+    toks = cg.run_tokens(4242, n, S.VOCAB)
+    h = cg.prefix_hashes(toks, 1)
+    dev = "cuda"
+    q = torch.empty((n, hq, d), dtype=torch.bfloat16, device=dev)
+    kn = torch.empty((n, hkv, d), dtype=torch.bfloat16, device=dev)
+    vn = torch.empty_like(kn)
+    gpu_gen.fill(q, h, cg.STREAM_Q)
+    gpu_gen.fill(kn, h, cg.STREAM_K)
+    gpu_gen.fill(vn, h, cg.STREAM_V)
+    i32 = lambda a: torch.tensor(a, dtype=torch.int32, device=dev)  # noqa: E731
+    # recompute: every position is new
+    pool = torch.zeros((8, hkv, d), dtype=torch.bfloat16, device=dev)
+    full = pa.ra_extend_attention(q, kn, vn, pool, pool, i32([[0]]), i32([0]), i32([0]), i32([n]), i32([0]), n,
+                                  1.0 / np.sqrt(d))
+    # reuse: the prefix sits in scattered pool slots
+    S_ = 4 * n
+    slots = np.random.default_rng(0).choice(S_, p, replace=False).astype(np.int32)
+    kp = torch.zeros((S_, hkv, d), dtype=torch.bfloat16, device=dev)
+    vp = torch.zeros_like(kp)
+    pa.ra_store_kv(torch.from_numpy(slots).cuda(), kn[:p].contiguous(), vn[:p].contiguous(), kp, vp)
+    part = pa.ra_extend_attention(q[p:].contiguous(), kn[p:].contiguous(), vn[p:].contiguous(), kp, vp,
+                                  torch.from_numpy(slots[None]).cuda(), i32([0]), i32([p]), i32([e]), i32([0]), e,
+                                  1.0 / np.sqrt(d))
+    torch.cuda.synchronize()
+    assert_close(_bf(part), _bf(full)[p:].astype(np.float64), "reuse vs recompute")
+    ref = oa.attend(cg.values(h[p:], cg.STREAM_Q, hq, d), cg.values(h, cg.STREAM_K, hkv, d),
+                    cg.values(h, cg.STREAM_V, hkv, d), np.arange(p, n), 1.0 / np.sqrt(np.float32(d)))
+    assert_close(_bf(part), ref, "reuse vs oracle")
+
+
+def test_empty_and_invalid_arguments():
+    log("case: empty batch and argument errors")
+    z = torch.zeros((4, 2, 64), dtype=torch.bfloat16, device="cuda")
+    t = torch.zeros((1, 4), dtype=torch.int32, device="cuda")
+    e = torch.zeros((0,), dtype=torch.int32, device="cuda")
+    out = pa.ra_decode_attention(z[:0], z, z, t, e, e, 4, 0.125)
+    assert out.shape[0] == 0
+    with pytest.raises(pa.RadixAttnError):
+        pa.ra_decode_attention(torch.zeros((1, 3, 64), dtype=torch.bfloat16, device="cuda"), z, z, t,
+                               torch.zeros(1, dtype=torch.int32, device="cuda"),
+                               torch.ones(1, dtype=torch.int32, device="cuda"), 4, 0.125)
+    with pytest.raises(pa.RadixAttnError):  # G = 3 not a power of two for extend
+        pa.ra_extend_attention(torch.zeros((1, 6, 64), dtype=torch.bfloat16, device="cuda"), z[:1], z[:1], z, z, t,
+                               torch.zeros(1, dtype=torch.int32, device="cuda"),
+                               torch.zeros(1, dtype=torch.int32, device="cuda"),
+                               torch.ones(1, dtype=torch.int32, device="cuda"),
+                               torch.zeros(1, dtype=torch.int32, device="cuda"), 1, 0.125)
