@@ -1,28 +1,51 @@
 // Decode attention over the token-granular KV pool: one query token per
 // request over its whole context (prefix plus private suffix), read through
 // the request's row of the slot table.  Decode dominates when outputs are
-// long (evaluation, section 6.2); it is bound by HBM bandwidth.
+// long (evaluation, section 6.2); it is bound by HBM bandwidth, so the design
+// goal is a steady stream of gathered 256-byte K/V rows.
 //
-// Work item = (request, kv head, KV chunk); one wave per item.  The G query
-// heads that share a kv head are the N = 16 columns of bf16 MFMAs, so every
-// K/V row fetched from HBM serves all G heads and the VALU is left for the
-// softmax:
-//   S^T[token, head] = K[token, :] . Q[head, :]   (A = gathered K rows, loaded
-//                                                  straight into registers)
-//   O^T[d, head]    += V^T[d, token] P^T[token, head]
-// V^T is staged through LDS (each lane writes its gathered 16-byte V piece
-// transposed).  Online softmax in the base-2 domain: the running maximum is
-// reduced across the four 16-lane rows with lane shuffles; the running sum
-// stays per lane and is reduced once at the end.  A chunk writes a normalised
-// partial output and its log-sum-exp; a second kernel merges the chunks.
+// Work item = (request, kv head, KV chunk); one wave per item.
+//   * Gather: every 32-token tile's K and V rows are copied HBM -> LDS with
+//     direct-to-LDS loads (global_load_lds_dwordx4), kNS tiles deep, no VGPR
+//     staging; the slot indices travel the same way one tile further ahead,
+//     so no load waits on an index.  Rows are unpadded (2*D bytes) with their
+//     16-byte pieces XOR-swizzled by swz(row) to spread LDS banks.
+//   * The G query heads that share the kv head are the N = 16 columns of
+//     bf16 MFMAs, so each K/V row fetched serves all G heads and the VALU is
+//     left for the softmax:  S^T[token, head] = K Q^T, O^T += V^T P^T, V^T
+//     read from the row-major LDS tile with ds_read_b64_tr_b16.
+//   * Online softmax in the base-2 domain with a lazily moved maximum; the
+//     maximum is reduced across the four 16-lane rows with permlane swaps,
+//     the sum stays per lane and is reduced once at the end.
+// A chunk writes a normalised partial output and its log2-sum-exp; a second
+// kernel merges the chunks.  DMAs are issued from inline assembly (the
+// compiler would wait for them before every LDS read); waits are explicit.
 #include "device_common.h"
 
 namespace {
 
-constexpr int kTile = 32;          // tokens per MFMA step (two 16-row blocks)
-constexpr int kVtPitch = 40;       // LDS row pitch of V^T in bf16 (32 + 8 pad)
+constexpr int kTile = 32;  // tokens per tile (two 16-row MFMA blocks)
+constexpr int kNS = 3;     // tiles in flight per wave
 
 __device__ __forceinline__ uint4 ld16(const __bf16* p) { return *reinterpret_cast<const uint4*>(p); }
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return static_cast<uint32_t>(reinterpret_cast<uintptr_t>(p));
+}
+__device__ __forceinline__ void dma16(const void* g, uint32_t lds_base) {
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds_base) : "memory");
+}
+__device__ __forceinline__ void dma4(const void* g, uint32_t lds_base) {
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dword %0, off" ::"v"(g), "s"(lds_base) : "memory");
+}
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | 0x0F70);
+}
+template <int PIECES>
+__device__ __forceinline__ int swz(int row) {
+  return (row ^ ((row >> 4) << 2)) & (PIECES - 1);
+}
 
 template <int D>
 __global__ __launch_bounds__(64) void decode_partial_kernel(
@@ -31,9 +54,15 @@ __global__ __launch_bounds__(64) void decode_partial_kernel(
     const int32_t* __restrict__ req_pool_idx, const int32_t* __restrict__ seq_lens, int32_t batch,
     int32_t hkv, int32_t grp, int32_t chunk_len, int32_t max_splits, int32_t max_len, float scale_log2,
     float* __restrict__ ws_o, float* __restrict__ ws_lse, __bf16* __restrict__ out) {
-  constexpr int KS = D / 32;  // MFMA k-steps over the head dimension
-  constexpr int DB = D / 16;  // 16-row blocks of O^T
-  __shared__ unsigned short vt[D * kVtPitch];
+  constexpr int KS = D / 32;            // MFMA k-steps over the head dimension
+  constexpr int DB = D / 16;            // 16-row blocks of O^T
+  constexpr int PIECES = D / 8;         // 16-byte pieces per row
+  constexpr int ROWB = 2 * D;           // bytes per row
+  constexpr int TILE_B = kTile * ROWB;  // bytes per K (or V) tile
+  constexpr int LOADS = TILE_B / 1024;  // DMA instructions per tile per tensor
+  constexpr int RING = kNS + 1;
+  __shared__ __align__(16) unsigned char kv_lds[kNS][2][TILE_B];
+  __shared__ __align__(16) int32_t idx_lds[RING][64];
 
   const int item = blockIdx.x;
   const int b = item % batch;
@@ -48,12 +77,42 @@ __global__ __launch_bounds__(64) void decode_partial_kernel(
   const int t_end = min(L, t_begin + chunk_len);
   int64_t rrow = req_pool_idx[b];
   rrow = (rrow >= 0 && rrow < rtt_rows) ? rrow : 0;
-  const int64_t row = rrow * rtt_stride;
+  const int32_t* trow = rtt + rrow * rtt_stride;
   const int hq = hkv * grp;
+  const int n_tiles = (t_end - t_begin + kTile - 1) / kTile;
 
   const int lane = threadIdx.x;
-  const int c = lane & 15;   // query head column / token row of the A operand
-  const int g4 = lane >> 4;  // which 8-wide k slice this lane holds
+  const int c = lane & 15;   // query head column / A-operand row
+  const int g4 = lane >> 4;  // which 16-lane row of the wave
+
+  auto issue_idx = [&](int tile) {
+    if (tile >= n_tiles) return;
+    int pos = t_begin + tile * kTile + (lane & 31);
+    pos = pos < t_end ? pos : t_end - 1;  // padding rows repeat a real token
+    dma4(trow + pos, lds_addr(&idx_lds[tile % RING][0]));
+  };
+  auto issue_kv = [&](int tile) {
+    if (tile >= n_tiles) return;
+    const int32_t* ring = idx_lds[tile % RING];
+    unsigned char* kst = kv_lds[tile % kNS][0];
+    unsigned char* vst = kv_lds[tile % kNS][1];
+#pragma unroll
+    for (int ch = 0; ch < LOADS; ++ch) {
+      const int u = (ch * 64 + lane) / PIECES;  // token row within the tile
+      const int pc = (lane % PIECES) ^ swz<PIECES>(u);
+      int64_t s = ring[u];
+      s = (s >= 0 && s < pool_slots) ? s : 0;
+      const int64_t off = (s * hkv + g) * D + 8 * pc;
+      dma16(k_pool + off, __builtin_amdgcn_readfirstlane(lds_addr(kst + ch * 1024)));
+      dma16(v_pool + off, __builtin_amdgcn_readfirstlane(lds_addr(vst + ch * 1024)));
+    }
+  };
+
+  // prologue: indices for kNS tiles, K/V for kNS - 1
+  for (int t = 0; t < kNS; ++t) issue_idx(t);
+  wait_vmcnt<0>();
+  __syncthreads();
+  for (int t = 0; t < kNS - 1; ++t) issue_kv(t);
 
   // Q^T as the B operand: column c = head g*grp + c, k = 8*g4 .. of each step.
   bf16x8_t qt[KS];
@@ -61,105 +120,100 @@ __global__ __launch_bounds__(64) void decode_partial_kernel(
     const bool has = c < grp;
     const __bf16* qp = q + (static_cast<int64_t>(b) * hq + g * grp + (has ? c : 0)) * D + 8 * g4;
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      uint4 w = has ? ld16(qp + 32 * ks) : make_uint4(0, 0, 0, 0);
-      qt[ks] = __builtin_bit_cast(bf16x8_t, w);
-    }
+    for (int ks = 0; ks < KS; ++ks)
+      qt[ks] = __builtin_bit_cast(bf16x8_t, has ? ld16(qp + 32 * ks) : make_uint4(0, 0, 0, 0));
   }
 
   f32x4_t o[DB];
 #pragma unroll
   for (int i = 0; i < DB; ++i) o[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  float m_run = -INFINITY;
+  float m_run = -INFINITY;  // raw score units
   float l_run = 0.f;
+  // A-operand row c of S^T block bb is token 8 (c >> 2) + 4 bb + (c & 3), so
+  // that the accumulator's row group g4 holds tokens 8 g4 .. 8 g4 + 7: P^T's
+  // B-operand k slots in natural token order.
+  int krow[2];
+#pragma unroll
+  for (int bb = 0; bb < 2; ++bb) krow[bb] = 8 * (c >> 2) + 4 * bb + (c & 3);
 
-  const int64_t head_off = static_cast<int64_t>(g) * D + 8 * g4;
-  const int64_t row_elems = static_cast<int64_t>(hkv) * D;
-  // transposed-write column of this lane's two tokens (see P^T k-slot order)
-  const int col_a = 8 * (c >> 2) + (c & 3);
-  const int col_b = col_a + 4;
+  for (int t = 0; t < n_tiles; ++t) {
+    if (t + 1 < n_tiles) {
+      wait_vmcnt<2 * LOADS>();  // tile t and the index tile t+kNS-1 have landed
+    } else {
+      wait_vmcnt<0>();
+    }
+    __syncthreads();
+    issue_idx(t + kNS);
+    issue_kv(t + kNS - 1);
 
-  for (int t0 = t_begin; t0 < t_end; t0 += kTile) {
-    const int ta = t0 + c, tb = t0 + 16 + c;
-    const bool va = ta < t_end, vb = tb < t_end;
-    int64_t sa = va ? rtt[row + ta] : 0;
-    int64_t sb = vb ? rtt[row + tb] : 0;
-    sa = (sa >= 0 && sa < pool_slots) ? sa : 0;
-    sb = (sb >= 0 && sb < pool_slots) ? sb : 0;
-    const __bf16* kpa = k_pool + sa * row_elems + head_off;
-    const __bf16* kpb = k_pool + sb * row_elems + head_off;
-    const __bf16* vpa = v_pool + sa * row_elems + head_off;
-    const __bf16* vpb = v_pool + sb * row_elems + head_off;
-    uint4 ka[KS], kb[KS], wa[KS], wb[KS];
-    const uint4 z = make_uint4(0, 0, 0, 0);
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      ka[ks] = va ? ld16(kpa + 32 * ks) : z;
-      kb[ks] = vb ? ld16(kpb + 32 * ks) : z;
-    }
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      wa[ks] = va ? ld16(vpa + 32 * ks) : z;
-      wb[ks] = vb ? ld16(vpb + 32 * ks) : z;
-    }
+    const unsigned char* kst = kv_lds[t % kNS][0];
+    const unsigned char* vst = kv_lds[t % kNS][1];
+    const int t0 = t_begin + t * kTile;
 
-    // S^T for tokens t0 + 4*g4 + i (sA) and t0 + 16 + 4*g4 + i (sB), head c.
-    f32x4_t sA = {0.f, 0.f, 0.f, 0.f}, sB = {0.f, 0.f, 0.f, 0.f};
+    f32x4_t sacc[2];
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      sA = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, ka[ks]), qt[ks], sA, 0, 0, 0);
-      sB = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, kb[ks]), qt[ks], sB, 0, 0, 0);
-    }
-    float s[8];
-    float mt = -INFINITY;
+    for (int bb = 0; bb < 2; ++bb) {
+      sacc[bb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+      const unsigned char* rp = kst + krow[bb] * ROWB;
+      const int sw = swz<PIECES>(krow[bb]);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int tA = t0 + 4 * g4 + i, tB = t0 + 16 + 4 * g4 + i;
-      s[i] = tA < t_end ? sA[i] * scale_log2 : -INFINITY;
-      s[4 + i] = tB < t_end ? sB[i] * scale_log2 : -INFINITY;
-      mt = fmaxf(mt, fmaxf(s[i], s[4 + i]));
-    }
-    mt = ra_max_across_rows(mt);
-    const float m_new = fmaxf(m_run, mt);
-    const float alpha = ra_exp2(m_run - m_new);
-    float psum = 0.f;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      s[i] = ra_exp2(s[i] - m_new);
-      psum += s[i];
-    }
-    l_run = l_run * alpha + psum;
-    m_run = m_new;
-#pragma unroll
-    for (int i = 0; i < DB; ++i) o[i] *= alpha;
-    uint4 pw;
-    pw.x = ra_pack_bf16x2(s[0], s[1]);
-    pw.y = ra_pack_bf16x2(s[2], s[3]);
-    pw.z = ra_pack_bf16x2(s[4], s[5]);
-    pw.w = ra_pack_bf16x2(s[6], s[7]);
-    const bf16x8_t pt = __builtin_bit_cast(bf16x8_t, pw);
-
-    // V^T into LDS: element (d, k-slot); this lane holds d = 32ks + 8g4 + e.
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      const uint32_t a4[4] = {wa[ks].x, wa[ks].y, wa[ks].z, wa[ks].w};
-      const uint32_t b4[4] = {wb[ks].x, wb[ks].y, wb[ks].z, wb[ks].w};
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int d0 = 32 * ks + 8 * g4 + 2 * e;
-        vt[d0 * kVtPitch + col_a] = static_cast<unsigned short>(a4[e] & 0xFFFFu);
-        vt[(d0 + 1) * kVtPitch + col_a] = static_cast<unsigned short>(a4[e] >> 16);
-        vt[d0 * kVtPitch + col_b] = static_cast<unsigned short>(b4[e] & 0xFFFFu);
-        vt[(d0 + 1) * kVtPitch + col_b] = static_cast<unsigned short>(b4[e] >> 16);
+      for (int ks = 0; ks < KS; ++ks) {
+        const int pc = (4 * ks + g4) ^ sw;
+        const bf16x8_t a = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const uint4*>(rp + 16 * pc));
+        sacc[bb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qt[ks], sacc[bb], 0, 0, 0);
       }
     }
-    __syncthreads();
+    // element (bb, i) is token t0 + 8 g4 + 4 bb + i
+    if (t0 + kTile > t_end) {
+#pragma unroll
+      for (int bb = 0; bb < 2; ++bb)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          if (t0 + 8 * g4 + 4 * bb + i >= t_end) sacc[bb][i] = -INFINITY;
+    }
+    float mt = fmaxf(fmaxf(fmaxf(sacc[0][0], sacc[0][1]), fmaxf(sacc[0][2], sacc[0][3])),
+                     fmaxf(fmaxf(sacc[1][0], sacc[1][1]), fmaxf(sacc[1][2], sacc[1][3])));
+    mt = ra_max_across_rows(mt);
+    if (__builtin_amdgcn_ballot_w64((mt - m_run) * scale_log2 > 8.f) != 0) {
+      const float m_new = fmaxf(m_run, mt);
+      const float alpha = ra_exp2((m_run - m_new) * scale_log2);
+      l_run *= alpha;
+#pragma unroll
+      for (int i = 0; i < DB; ++i) o[i] *= alpha;
+      m_run = m_new;
+    }
+    const float mb = -m_run * scale_log2;
+    float p[8];
+#pragma unroll
+    for (int bb = 0; bb < 2; ++bb)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        p[4 * bb + i] = ra_exp2(__builtin_fmaf(sacc[bb][i], scale_log2, mb));
+        l_run += p[4 * bb + i];
+      }
+    uint4 pw;
+    pw.x = ra_pack_bf16x2(p[0], p[1]);
+    pw.y = ra_pack_bf16x2(p[2], p[3]);
+    pw.z = ra_pack_bf16x2(p[4], p[5]);
+    pw.w = ra_pack_bf16x2(p[6], p[7]);
+    const bf16x8_t pt = __builtin_bit_cast(bf16x8_t, pw);
+
+    // O^T += V^T P^T: lane (c, g4) supplies row 8 g4 + 4 h + (c >> 2),
+    // columns 16 db + 4 (c & 3) .. +3, and receives column 16 db + c of rows
+    // 8 g4 + 4 h + 0..3.
 #pragma unroll
     for (int db = 0; db < DB; ++db) {
-      const uint4 a = *reinterpret_cast<const uint4*>(&vt[(16 * db + c) * kVtPitch + 8 * g4]);
-      o[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a), pt, o[db], 0, 0, 0);
+      bf16x4_t half[2];
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int r = 8 * g4 + 4 * h + (c >> 2);
+        const int pc = (2 * db + ((c & 3) >> 1)) ^ swz<PIECES>(r);
+        half[h] = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+            (__attribute__((address_space(3))) bf16x4_t*)(vst + r * ROWB + 16 * pc + 8 * (c & 1)));
+      }
+      const bf16x8_t a = __builtin_shufflevector(half[0], half[1], 0, 1, 2, 3, 4, 5, 6, 7);
+      o[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pt, o[db], 0, 0, 0);
     }
-    __syncthreads();
   }
 
   const float l_tot = ra_sum_across_rows(l_run);
@@ -183,7 +237,7 @@ __global__ __launch_bounds__(64) void decode_partial_kernel(
       *reinterpret_cast<float4*>(wp + 16 * db) =
           make_float4(o[db][0] * inv, o[db][1] * inv, o[db][2] * inv, o[db][3] * inv);
     }
-    if (g4 == 0) ws_lse[pidx] = m_run + __log2f(l_tot);
+    if (g4 == 0) ws_lse[pidx] = m_run * scale_log2 + __log2f(l_tot);
   }
 }
 
@@ -234,8 +288,8 @@ extern "C" int32_t ra_decode_chunk_len(int32_t batch, int32_t hkv, int32_t max_s
     int64_t c = ceil_div(max_seq_len, num_splits);
     return static_cast<int32_t>(ceil_div(c, kTile) * kTile);
   }
-  // Largest chunk that still gives enough work items to fill the chip
-  // (256 CUs x 4 SIMDs, several waves each).
+  // Largest chunk that still gives enough work items to keep every CU
+  // streaming (256 CUs, a few waves each, several rounds for balance).
   const int64_t target = 4096;
   for (int32_t c : {2048, 1024, 512}) {
     if (static_cast<int64_t>(batch) * hkv * ceil_div(max_seq_len, c) >= target) return c;
@@ -254,12 +308,13 @@ extern "C" size_t ra_decode_workspace_bytes(int32_t batch, int32_t hq, int32_t h
 
 extern "C" int ra_decode_attention(const void* q, const void* k_pool, const void* v_pool, int64_t pool_slots,
                                    const int32_t* req_to_token, int64_t rtt_rows, int64_t rtt_stride,
-                                   const int32_t* req_pool_idx, const int32_t* seq_lens, int32_t batch, int32_t max_seq_len, int32_t hq,
-                                   int32_t hkv, int32_t d, float scale, int32_t num_splits, void* workspace,
-                                   size_t workspace_bytes, void* out, hipStream_t stream) {
+                                   const int32_t* req_pool_idx, const int32_t* seq_lens, int32_t batch,
+                                   int32_t max_seq_len, int32_t hq, int32_t hkv, int32_t d, float scale,
+                                   int32_t num_splits, void* workspace, size_t workspace_bytes, void* out,
+                                   hipStream_t stream) {
   if (batch < 0 || hq <= 0 || hkv <= 0 || hq % hkv != 0 || (d != 64 && d != 128) || pool_slots <= 0 ||
-      rtt_stride <= 0 || rtt_rows <= 0 || num_splits < 0)
-    return ra_fail(RA_EINVAL, "ra_decode_attention: bad sizes");
+      rtt_stride <= 0 || rtt_rows <= 0 || num_splits < 0 || !(scale > 0.f))
+    return ra_fail(RA_EINVAL, "ra_decode_attention: bad sizes or scale");
   const int32_t grp = hq / hkv;
   if (grp > 16) return ra_fail(RA_EINVAL, "ra_decode_attention: more than 16 query heads per kv head");
   if (batch == 0) return ra_ok();
@@ -287,12 +342,12 @@ extern "C" int ra_decode_attention(const void* q, const void* k_pool, const void
   auto* op = static_cast<__bf16*>(out);
   if (d == 128) {
     hipLaunchKernelGGL(decode_partial_kernel<128>, dim3(static_cast<uint32_t>(items)), dim3(64), 0, stream, qp,
-                       kp, vp, pool_slots, req_to_token, rtt_rows, rtt_stride, req_pool_idx, seq_lens, batch, hkv, grp,
-                       chunk, max_splits, max_seq_len, scale_log2, ws_o, ws_lse, op);
+                       kp, vp, pool_slots, req_to_token, rtt_rows, rtt_stride, req_pool_idx, seq_lens, batch, hkv,
+                       grp, chunk, max_splits, max_seq_len, scale_log2, ws_o, ws_lse, op);
   } else {
     hipLaunchKernelGGL(decode_partial_kernel<64>, dim3(static_cast<uint32_t>(items)), dim3(64), 0, stream, qp,
-                       kp, vp, pool_slots, req_to_token, rtt_rows, rtt_stride, req_pool_idx, seq_lens, batch, hkv, grp,
-                       chunk, max_splits, max_seq_len, scale_log2, ws_o, ws_lse, op);
+                       kp, vp, pool_slots, req_to_token, rtt_rows, rtt_stride, req_pool_idx, seq_lens, batch, hkv,
+                       grp, chunk, max_splits, max_seq_len, scale_log2, ws_o, ws_lse, op);
   }
   int st = ra_check_launch("ra_decode_attention(partial)");
   if (st != RA_OK || splits <= 1) return st;

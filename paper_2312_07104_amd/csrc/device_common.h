@@ -18,29 +18,35 @@ typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ float ra_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
-// Packs two fp32 into two bf16 (round to nearest even) in one 32-bit word:
-// low half from a, high half from b.
+// Packs two fp32 into two bf16 (round to nearest even, v_cvt_pk_bf16_f32) in
+// one 32-bit word: low half from a, high half from b.
 __device__ __forceinline__ uint32_t ra_pack_bf16x2(float a, float b) {
-  uint32_t ua = __builtin_bit_cast(uint32_t, a);
-  uint32_t ub = __builtin_bit_cast(uint32_t, b);
-  ua = (ua + 0x7FFFu + ((ua >> 16) & 1u)) >> 16;
-  ub = (ub + 0x7FFFu + ((ub >> 16) & 1u)) & 0xFFFF0000u;
-  return ua | ub;
+  typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+  const bf16x2_t v = {static_cast<__bf16>(a), static_cast<__bf16>(b)};
+  return __builtin_bit_cast(uint32_t, v);
 }
 
 __device__ __forceinline__ float ra_bf16_lo(uint32_t w) { return __builtin_bit_cast(float, w << 16); }
 __device__ __forceinline__ float ra_bf16_hi(uint32_t w) { return __builtin_bit_cast(float, w & 0xFFFF0000u); }
 
-// Maximum over the four lanes that share (lane & 15): lanes l, l^16, l^32, l^48.
+// Reductions over the four lanes that share (lane & 15): lanes l, l^16, l^32,
+// l^48.  v_permlane32_swap / v_permlane16_swap exchange 32- / 16-lane halves
+// of a register pair, so each step is one swap and one VALU op.
 __device__ __forceinline__ float ra_max_across_rows(float v) {
-  v = fmaxf(v, __shfl_xor(v, 16));
-  v = fmaxf(v, __shfl_xor(v, 32));
-  return v;
+  uint32_t u = __builtin_bit_cast(uint32_t, v);
+  auto r = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  v = fmaxf(__builtin_bit_cast(float, static_cast<uint32_t>(r[0])), __builtin_bit_cast(float, static_cast<uint32_t>(r[1])));
+  u = __builtin_bit_cast(uint32_t, v);
+  r = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+  return fmaxf(__builtin_bit_cast(float, static_cast<uint32_t>(r[0])), __builtin_bit_cast(float, static_cast<uint32_t>(r[1])));
 }
 __device__ __forceinline__ float ra_sum_across_rows(float v) {
-  v += __shfl_xor(v, 16);
-  v += __shfl_xor(v, 32);
-  return v;
+  uint32_t u = __builtin_bit_cast(uint32_t, v);
+  auto r = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  v = __builtin_bit_cast(float, static_cast<uint32_t>(r[0])) + __builtin_bit_cast(float, static_cast<uint32_t>(r[1]));
+  u = __builtin_bit_cast(uint32_t, v);
+  r = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+  return __builtin_bit_cast(float, static_cast<uint32_t>(r[0])) + __builtin_bit_cast(float, static_cast<uint32_t>(r[1]));
 }
 
 inline int ra_check_launch(const char* who) {

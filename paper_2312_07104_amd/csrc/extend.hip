@@ -1,23 +1,35 @@
 // Extend attention: prefill of a request's new tokens over its cached prefix
 // (the work that remains once RadixAttention has reused the prefix's KV
 // cache; section 3, Appendix A.1), plus causal attention among the new
-// tokens.  This is a dense contraction, so QK^T and PV run on bf16 MFMA with
-// fp32 accumulation.
+// tokens.  This is a dense contraction, so QK^T and PV run on bf16 MFMA
+// (v_mfma_f32_16x16x32_bf16) with fp32 accumulation.
 //
-// Work item = (request, kv head, query tile).  A tile holds 128 query rows,
+// Work item = (request, kv head, query tile).  A tile holds 128 query rows
 // packed as (new token, query head of the kv head's group): the G heads that
-// share a kv head share every K/V tile the work-group stages.  Four waves,
-// 32 rows each; per 64-key tile:
-//   * all 256 threads gather the next tile's K and V rows into registers
-//     (prefix keys through the request's slot-table row, new keys from the
-//     contiguous k_new / v_new rows) while the current tile is computed;
-//   * K goes to LDS row-major, V transposed (so PV's k dimension is
-//     contiguous per lane);
-//   * S^T[key, query] = K Q^T with the queries as MFMA columns, so each
-//     lane ends up owning one query column and the row max / row sum are
-//     in-lane plus two cross-row shuffles;
-//   * P^T stays in registers as the B operand of O^T += V^T P^T.
-// Masking only runs on tiles that reach past the first query's last key.
+// share a kv head share every K/V tile the work-group stages.  Four waves of
+// 32 rows.  Per 64-key tile:
+//   * K and V rows are copied HBM -> LDS by direct-to-LDS loads
+//     (global_load_lds_dwordx4), no VGPR staging.  Prefix keys are gathered
+//     through the request's slot-table row, new keys come from the contiguous
+//     k_new / v_new rows.  The slot indices themselves travel by DMA into a
+//     small LDS ring two tiles ahead, so a tile's gather never waits on its
+//     index load.  The K/V ring has NS stages.
+//   * A DMA writes lane i's 16 bytes at base + 16 i, so rows sit unpadded at
+//     2*D bytes; the 16-byte pieces of row r are XOR-swizzled by swz(r) (the
+//     source address picks the piece) to spread LDS banks.
+//   * S^T[key, query] = K Q^T with the queries as the MFMA columns: each lane
+//     owns one query column, so the row max / row sum are in-lane plus two
+//     cross-row shuffles.  K rows are fed to the A operand in the order that
+//     makes the accumulator's four 16-lane row groups hold keys 8g..8g+7 of
+//     each 32-key step, which is exactly P^T's B-operand layout.
+//   * O^T += V^T P^T: V stays row-major in LDS; ds_read_b64_tr_b16 reads it
+//     transposed (lane i of a 16-lane group gets column i of four rows), two
+//     reads per A operand.
+// The DMAs are issued from inline assembly: the compiler would otherwise
+// wait for every outstanding DMA before each LDS read, serialising the
+// pipeline.  Waits are explicit s_waitcnt vmcnt at the top of each tile.
+#include <cstdlib>
+
 #include "device_common.h"
 
 namespace {
@@ -27,38 +39,62 @@ constexpr int kBN = 64;   // keys per tile
 
 __device__ __forceinline__ uint4 ld16(const __bf16* p) { return *reinterpret_cast<const uint4*>(p); }
 
-// Column of key u (0..63) in the transposed V tile.  Inside each 32-key MFMA
-// step, the P^T operand of lane group g4 holds keys 4g4..4g4+3 then
-// 16+4g4..16+4g4+3 (the S^T accumulator layout), so V^T stores them in
-// that order.
-__device__ __forceinline__ int vt_col(int u) {
-  const int w = u & 31;
-  return (u & 32) + 8 * ((w & 15) >> 2) + (w & 3) + ((w & 16) ? 4 : 0);
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return static_cast<uint32_t>(reinterpret_cast<uintptr_t>(p));
 }
 
-template <int D>
-__global__ __launch_bounds__(256, 2) void extend_kernel(
+// Direct global -> LDS copies: lane i's data lands at lds_base + size * i.
+__device__ __forceinline__ void dma16(const void* g, uint32_t lds_base) {
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds_base) : "memory");
+}
+__device__ __forceinline__ void dma4(const void* g, uint32_t lds_base) {
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dword %0, off" ::"v"(g), "s"(lds_base) : "memory");
+}
+
+// s_waitcnt vmcnt(n) with expcnt / lgkmcnt left unconstrained (gfx9 layout).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | 0x0F70);
+}
+
+template <int PIECES>
+__device__ __forceinline__ int swz(int row) {
+  return (row ^ ((row >> 4) << 2)) & (PIECES - 1);
+}
+
+template <int D, int NS>
+__global__ __launch_bounds__(256, NS == 2 ? 2 : 1) void extend_kernel(
     const __bf16* __restrict__ q, const __bf16* __restrict__ k_new, const __bf16* __restrict__ v_new,
     int64_t total_tokens, const __bf16* __restrict__ k_pool, const __bf16* __restrict__ v_pool,
     int64_t pool_slots, const int32_t* __restrict__ rtt, int64_t rtt_rows, int64_t rtt_stride,
     const int32_t* __restrict__ req_pool_idx, const int32_t* __restrict__ prefix_lens,
     const int32_t* __restrict__ extend_lens, const int32_t* __restrict__ extend_start, int32_t batch,
     int32_t hkv, int32_t grp, int32_t n_qtiles, float scale_log2, __bf16* __restrict__ out) {
-  constexpr int KS = D / 32;              // MFMA k-steps over the head dimension
-  constexpr int DB = D / 16;              // 16-row blocks of O^T
-  constexpr int KP = D + 8;               // K tile pitch (bf16)
-  constexpr int VP = kBN + 8;             // V^T tile pitch (bf16)
-  constexpr int PIECES = D / 8;           // 16-byte pieces per row
-  constexpr int LOADS = kBN * PIECES / 256;
-  __shared__ __align__(16) unsigned short k_lds[kBN * KP];
-  __shared__ __align__(16) unsigned short vt_lds[D * VP];
+  constexpr int KS = D / 32;                  // MFMA k-steps over the head dimension
+  constexpr int DB = D / 16;                  // 16-row blocks of O^T
+  constexpr int PIECES = D / 8;               // 16-byte pieces per row
+  constexpr int ROWB = 2 * D;                 // bytes per K or V row
+  constexpr int TILE_B = kBN * ROWB;          // bytes per K (or V) tile
+  constexpr int LOADS = TILE_B / (256 * 16);  // DMA instructions per wave per tile per tensor
+  constexpr int RING = NS + 1;                // slot-index ring depth
+  __shared__ __align__(16) unsigned char kv_lds[NS][2][TILE_B];
+  __shared__ __align__(16) int32_t idx_lds[RING][kBN];
 
-  const int item = blockIdx.x;
-  const int b = item % batch;
-  const int rest = item / batch;
-  const int g = rest % hkv;
-  const int qt = n_qtiles - 1 - rest / hkv;  // longest tiles first
-  const int tpb = kBM / grp;                 // new tokens per tile
+  // Work-groups go to the 8 XCDs round-robin (block i -> XCD i % 8).  Items
+  // are ordered (kv head, request, query tile, longest tile first) and each
+  // XCD takes a contiguous eighth of that order, so the work-groups in flight
+  // on one XCD share a kv head and mostly one request: they stream the same
+  // K/V rows and hit that XCD's L2.
+  const int64_t n_items = static_cast<int64_t>(hkv) * batch * n_qtiles;
+  const int64_t per_xcd = (n_items + 7) / 8;
+  const int64_t item = static_cast<int64_t>(blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
+  if (item >= n_items) return;
+  const int g = static_cast<int>(item / (static_cast<int64_t>(batch) * n_qtiles));
+  const int rem = static_cast<int>(item % (static_cast<int64_t>(batch) * n_qtiles));
+  const int b = rem / n_qtiles;
+  const int qt = n_qtiles - 1 - rem % n_qtiles;
+  const int tpb = kBM / grp;  // new tokens per tile
 
   const int64_t start = extend_start[b];
   int64_t E = extend_lens[b];
@@ -73,12 +109,59 @@ __global__ __launch_bounds__(256, 2) void extend_kernel(
   const int32_t* trow = rtt + rrow * rtt_stride;
   const int kend = P + tok_end;
   const int hq = hkv * grp;
+  const int n_tiles = (kend + kBN - 1) / kBN;
 
   const int tid = threadIdx.x;
   const int wave = tid >> 6;
   const int lane = tid & 63;
   const int c = lane & 15;
   const int g4 = lane >> 4;
+
+  // ---- DMA issue helpers ---------------------------------------------------
+  auto issue_idx = [&](int tile) {  // wave 0 only: slot indices of one tile
+    const int kb = tile * kBN;
+    if (wave != 0 || tile >= n_tiles || kb >= P) return;
+    const int pos = kb + lane;
+    dma4(trow + (pos < P ? pos : 0), lds_addr(&idx_lds[tile % RING][0]));
+  };
+  auto issue_kv = [&](int tile) {
+    if (tile >= n_tiles) return;
+    const int kb = tile * kBN;
+    const int32_t* ring = idx_lds[tile % RING];
+    unsigned char* kst = kv_lds[tile % NS][0];
+    unsigned char* vst = kv_lds[tile % NS][1];
+#pragma unroll
+    for (int it = 0; it < LOADS; ++it) {
+      const int ch = it * 4 + wave;                // 1 KB chunk of the tile
+      const int u = (ch * 64 + lane) / PIECES;     // key row within the tile
+      const int pc = (lane % PIECES) ^ swz<PIECES>(u);
+      int pos = kb + u;
+      pos = pos < kend ? pos : kend - 1;           // padding rows repeat a real key
+      const __bf16* ks;
+      const __bf16* vs;
+      if (pos < P) {
+        int64_t s = ring[u];
+        s = (s >= 0 && s < pool_slots) ? s : 0;
+        const int64_t off = (s * hkv + g) * D + 8 * pc;
+        ks = k_pool + off;
+        vs = v_pool + off;
+      } else {
+        const int64_t off = ((start + pos - P) * hkv + g) * D + 8 * pc;
+        ks = k_new + off;
+        vs = v_new + off;
+      }
+      const uint32_t kb_lds = __builtin_amdgcn_readfirstlane(lds_addr(kst + ch * 1024));
+      const uint32_t vb_lds = __builtin_amdgcn_readfirstlane(lds_addr(vst + ch * 1024));
+      dma16(ks, kb_lds);
+      dma16(vs, vb_lds);
+    }
+  };
+
+  // ---- prologue: indices for the first NS tiles, K/V for the first NS-1 ---
+  for (int t = 0; t < NS; ++t) issue_idx(t);
+  wait_vmcnt<0>();
+  __syncthreads();
+  for (int t = 0; t < NS - 1; ++t) issue_kv(t);
 
   // Q^T operands for the wave's two 16-query column blocks.
   bf16x8_t qT[2][KS];
@@ -104,116 +187,131 @@ __global__ __launch_bounds__(256, 2) void extend_kernel(
   float m_run[2] = {-INFINITY, -INFINITY};
   float l_run[2] = {0.f, 0.f};
 
-  // Tile gather into registers.
-  uint4 kreg[LOADS], vreg[LOADS];
-  auto load_tile = [&](int kbase) {
+  // Per-lane LDS offsets that do not depend on the tile.
+  // S^T block b of 32-key step k2 feeds A-operand row c with key
+  // 32 k2 + 8 (c >> 2) + 4 b + (c & 3).
+  int krow[2][2];
 #pragma unroll
-    for (int it = 0; it < LOADS; ++it) {
-      const int p = tid + 256 * it;
-      const int u = p / PIECES, pc = p % PIECES;
-      const int pos = kbase + u;
-      if (pos < kend) {
-        int64_t roff;
-        if (pos < P) {
-          int64_t s = trow[pos];
-          s = (s >= 0 && s < pool_slots) ? s : 0;
-          roff = (s * hkv + g) * D + 8 * pc;
-          kreg[it] = ld16(k_pool + roff);
-          vreg[it] = ld16(v_pool + roff);
-        } else {
-          roff = ((start + pos - P) * hkv + g) * D + 8 * pc;
-          kreg[it] = ld16(k_new + roff);
-          vreg[it] = ld16(v_new + roff);
-        }
-      } else {
-        kreg[it] = make_uint4(0, 0, 0, 0);
-        vreg[it] = make_uint4(0, 0, 0, 0);
-      }
-    }
-  };
-  auto store_tile = [&]() {
+  for (int k2 = 0; k2 < 2; ++k2)
 #pragma unroll
-    for (int it = 0; it < LOADS; ++it) {
-      const int p = tid + 256 * it;
-      const int u = p / PIECES, pc = p % PIECES;
-      *reinterpret_cast<uint4*>(&k_lds[u * KP + 8 * pc]) = kreg[it];
-      const int col = vt_col(u);
-      const uint32_t w[4] = {vreg[it].x, vreg[it].y, vreg[it].z, vreg[it].w};
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        vt_lds[(8 * pc + 2 * e) * VP + col] = static_cast<unsigned short>(w[e] & 0xFFFFu);
-        vt_lds[(8 * pc + 2 * e + 1) * VP + col] = static_cast<unsigned short>(w[e] >> 16);
-      }
-    }
-  };
+    for (int bb = 0; bb < 2; ++bb) krow[k2][bb] = 32 * k2 + 8 * (c >> 2) + 4 * bb + (c & 3);
 
-  const int n_tiles = (kend + kBN - 1) / kBN;
-  load_tile(0);
   for (int t = 0; t < n_tiles; ++t) {
     const int kbase = t * kBN;
-    __syncthreads();
-    store_tile();
-    __syncthreads();
-    if (t + 1 < n_tiles) load_tile(kbase + kBN);
-
-    // S^T blocks: 4 key blocks x 2 query blocks.
-    f32x4_t sacc[4][2];
-#pragma unroll
-    for (int tb = 0; tb < 4; ++tb) {
-      sacc[tb][0] = sacc[tb][1] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        const bf16x8_t a =
-            __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const uint4*>(&k_lds[(16 * tb + c) * KP + 32 * ks + 8 * g4]));
-        sacc[tb][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qT[0][ks], sacc[tb][0], 0, 0, 0);
-        sacc[tb][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qT[1][ks], sacc[tb][1], 0, 0, 0);
-      }
+    if (NS == 2 || t + 1 >= n_tiles) {
+      wait_vmcnt<0>();
+    } else {
+      wait_vmcnt<2 * LOADS>();
     }
-    const bool need_mask = kbase + kBN - 1 > P + tok0;
-    bf16x8_t pT[2][2];  // [k-step][query block]
+    __syncthreads();
+    issue_idx(t + NS);
+    issue_kv(t + NS - 1);
+
+    const unsigned char* kst = kv_lds[t % NS][0];
+    const unsigned char* vst = kv_lds[t % NS][1];
+
+    // S^T: key blocks (k2, bb) x query blocks j.
+    f32x4_t sacc[2][2][2];
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      float s[16];
-      float mt = -INFINITY;
+    for (int k2 = 0; k2 < 2; ++k2) {
 #pragma unroll
-      for (int tb = 0; tb < 4; ++tb) {
+      for (int bb = 0; bb < 2; ++bb) {
+        sacc[k2][bb][0] = sacc[k2][bb][1] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        const int r = krow[k2][bb];
+        const unsigned char* rp = kst + r * ROWB;
+        const int sw = swz<PIECES>(r);
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          float v = sacc[tb][j][i] * scale_log2;
-          if (need_mask && kbase + 16 * tb + 4 * g4 + i > qlim[j]) v = -INFINITY;
-          s[4 * tb + i] = v;
-          mt = fmaxf(mt, v);
+        for (int ks = 0; ks < KS; ++ks) {
+          const int pc = (4 * ks + g4) ^ sw;
+          const bf16x8_t a = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const uint4*>(rp + 16 * pc));
+          sacc[k2][bb][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qT[0][ks], sacc[k2][bb][0], 0, 0, 0);
+          sacc[k2][bb][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qT[1][ks], sacc[k2][bb][1], 0, 0, 0);
         }
       }
+    }
+    // accumulator element (k2, bb, i) is key kbase + 32 k2 + 8 g4 + 4 bb + i.
+    // Online softmax in the base-2 domain with a lazily updated maximum: the
+    // running maximum (raw score units) only moves when some column's tile
+    // maximum exceeds it by more than 2^8 after scaling, so most tiles skip
+    // the rescale of O; exponentials stay <= 2^8, exact enough in fp32/bf16.
+    const bool need_mask = kbase + kBN - 1 > P + tok0;
+    bf16x8_t pT[2][2];  // [k2][query block]
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      float mt = -INFINITY;
+      if (need_mask) {
+#pragma unroll
+        for (int k2 = 0; k2 < 2; ++k2)
+#pragma unroll
+          for (int bb = 0; bb < 2; ++bb)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              if (kbase + 32 * k2 + 8 * g4 + 4 * bb + i > qlim[j]) sacc[k2][bb][j][i] = -INFINITY;
+            }
+      }
+#pragma unroll
+      for (int k2 = 0; k2 < 2; ++k2)
+#pragma unroll
+        for (int bb = 0; bb < 2; ++bb)
+          mt = fmaxf(mt, fmaxf(fmaxf(sacc[k2][bb][j][0], sacc[k2][bb][j][1]),
+                               fmaxf(sacc[k2][bb][j][2], sacc[k2][bb][j][3])));
       mt = ra_max_across_rows(mt);
-      const float m_new = fmaxf(m_run[j], mt);
-      const float alpha = ra_exp2(m_run[j] - m_new);
+      if (__builtin_amdgcn_ballot_w64((mt - m_run[j]) * scale_log2 > 8.f) != 0) {
+        const float m_new = fmaxf(m_run[j], mt);
+        const float alpha = ra_exp2((m_run[j] - m_new) * scale_log2);
+        l_run[j] *= alpha;
+#pragma unroll
+        for (int db = 0; db < DB; ++db) o[db][j] *= alpha;
+        m_run[j] = m_new;
+      }
+      const float mb = -m_run[j] * scale_log2;
       float psum = 0.f;
 #pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        s[i] = ra_exp2(s[i] - m_new);
-        psum += s[i];
-      }
-      l_run[j] = l_run[j] * alpha + psum;
-      m_run[j] = m_new;
-#pragma unroll
-      for (int db = 0; db < DB; ++db) o[db][j] *= alpha;
-#pragma unroll
       for (int k2 = 0; k2 < 2; ++k2) {
+        float p[8];
+#pragma unroll
+        for (int bb = 0; bb < 2; ++bb)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            p[4 * bb + i] = ra_exp2(__builtin_fmaf(sacc[k2][bb][j][i], scale_log2, mb));
+            psum += p[4 * bb + i];
+          }
         uint4 w;
-        w.x = ra_pack_bf16x2(s[8 * k2 + 0], s[8 * k2 + 1]);
-        w.y = ra_pack_bf16x2(s[8 * k2 + 2], s[8 * k2 + 3]);
-        w.z = ra_pack_bf16x2(s[8 * k2 + 4], s[8 * k2 + 5]);
-        w.w = ra_pack_bf16x2(s[8 * k2 + 6], s[8 * k2 + 7]);
+        w.x = ra_pack_bf16x2(p[0], p[1]);
+        w.y = ra_pack_bf16x2(p[2], p[3]);
+        w.z = ra_pack_bf16x2(p[4], p[5]);
+        w.w = ra_pack_bf16x2(p[6], p[7]);
         pT[k2][j] = __builtin_bit_cast(bf16x8_t, w);
       }
+      l_run[j] += psum;
     }
+    // O^T += V^T P^T.  Lane (c, g4) supplies row 32 k2 + 8 g4 + 4 h + (c >> 2),
+    // columns 16 db + 4 (c & 3) .. +3; it receives column 16 db + c of rows
+    // 32 k2 + 8 g4 + 4 h + 0..3.
 #pragma unroll
-    for (int db = 0; db < DB; ++db) {
+    for (int k2 = 0; k2 < 2; ++k2) {
+      int voff[2];
 #pragma unroll
-      for (int k2 = 0; k2 < 2; ++k2) {
-        const bf16x8_t a = __builtin_bit_cast(
-            bf16x8_t, *reinterpret_cast<const uint4*>(&vt_lds[(16 * db + c) * VP + 32 * k2 + 8 * g4]));
+      for (int h = 0; h < 2; ++h) {
+        const int r = 32 * k2 + 8 * g4 + 4 * h + (c >> 2);
+        voff[h] = r * ROWB + 8 * ((c & 3) & 1);
+      }
+#pragma unroll
+      for (int db = 0; db < DB; ++db) {
+        bf16x4_t lo, hi;
+        {
+          const int r = 32 * k2 + 8 * g4 + (c >> 2);
+          const int pc = (2 * db + ((c & 3) >> 1)) ^ swz<PIECES>(r);
+          lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+              (__attribute__((address_space(3))) bf16x4_t*)(vst + voff[0] + 16 * pc));
+        }
+        {
+          const int r = 32 * k2 + 8 * g4 + 4 + (c >> 2);
+          const int pc = (2 * db + ((c & 3) >> 1)) ^ swz<PIECES>(r);
+          hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+              (__attribute__((address_space(3))) bf16x4_t*)(vst + voff[1] + 16 * pc));
+        }
+        const bf16x8_t a = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
         o[db][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pT[k2][0], o[db][0], 0, 0, 0);
         o[db][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pT[k2][1], o[db][1], 0, 0, 0);
       }
@@ -234,6 +332,17 @@ __global__ __launch_bounds__(256, 2) void extend_kernel(
       *reinterpret_cast<uint2*>(op + 16 * db) = w;
     }
   }
+}
+
+template <int D, int NS>
+void launch(int64_t items, hipStream_t stream, const __bf16* qp, const __bf16* knp, const __bf16* vnp,
+            int64_t total_tokens, const __bf16* kp, const __bf16* vp, int64_t pool_slots, const int32_t* rtt,
+            int64_t rtt_rows, int64_t rtt_stride, const int32_t* rpi, const int32_t* pl, const int32_t* el,
+            const int32_t* es, int32_t batch, int32_t hkv, int32_t grp, int32_t n_qtiles, float scale_log2,
+            __bf16* op) {
+  hipLaunchKernelGGL((extend_kernel<D, NS>), dim3(static_cast<uint32_t>(items)), dim3(256), 0, stream, qp, knp, vnp,
+                     total_tokens, kp, vp, pool_slots, rtt, rtt_rows, rtt_stride, rpi, pl, el, es, batch, hkv, grp,
+                     n_qtiles, scale_log2, op);
 }
 
 }  // namespace
@@ -260,7 +369,7 @@ extern "C" int ra_extend_attention(const void* q, const void* k_new, const void*
     return ra_fail(RA_EINVAL, "ra_extend_attention: pointers must be 16-byte aligned");
   const int32_t tpb = kBM / grp;
   const int64_t n_qtiles = (static_cast<int64_t>(max_extend_len) + tpb - 1) / tpb;
-  const int64_t items = static_cast<int64_t>(batch) * hkv * n_qtiles;
+  const int64_t items = (static_cast<int64_t>(batch) * hkv * n_qtiles + 7) / 8 * 8;  // whole XCD rounds
   if (items > INT32_MAX) return ra_fail(RA_EINVAL, "ra_extend_attention: too many work items");
   const float scale_log2 = scale * RA_LOG2E;
   auto* qp = static_cast<const __bf16*>(q);
@@ -269,16 +378,20 @@ extern "C" int ra_extend_attention(const void* q, const void* k_new, const void*
   auto* kp = static_cast<const __bf16*>(k_pool);
   auto* vp = static_cast<const __bf16*>(v_pool);
   auto* op = static_cast<__bf16*>(out);
-  if (d == 128) {
-    hipLaunchKernelGGL(extend_kernel<128>, dim3(static_cast<uint32_t>(items)), dim3(256), 0, stream, qp, knp, vnp,
-                       total_tokens, kp, vp, pool_slots, req_to_token, rtt_rows, rtt_stride, req_pool_idx,
-                       prefix_lens, extend_lens, extend_start, batch, hkv, grp, static_cast<int32_t>(n_qtiles),
-                       scale_log2, op);
+  const int32_t nq = static_cast<int32_t>(n_qtiles);
+  static const int ns_env = [] { const char* e = getenv("RA_EXTEND_NS"); return e ? atoi(e) : 2; }();
+  if (d == 128 && ns_env == 3) {
+    launch<128, 3>(items, stream, qp, knp, vnp, total_tokens, kp, vp, pool_slots, req_to_token, rtt_rows,
+                   rtt_stride, req_pool_idx, prefix_lens, extend_lens, extend_start, batch, hkv, grp, nq,
+                   scale_log2, op);
+  } else if (d == 128) {
+    launch<128, 2>(items, stream, qp, knp, vnp, total_tokens, kp, vp, pool_slots, req_to_token, rtt_rows,
+                   rtt_stride, req_pool_idx, prefix_lens, extend_lens, extend_start, batch, hkv, grp, nq,
+                   scale_log2, op);
   } else {
-    hipLaunchKernelGGL(extend_kernel<64>, dim3(static_cast<uint32_t>(items)), dim3(256), 0, stream, qp, knp, vnp,
-                       total_tokens, kp, vp, pool_slots, req_to_token, rtt_rows, rtt_stride, req_pool_idx,
-                       prefix_lens, extend_lens, extend_start, batch, hkv, grp, static_cast<int32_t>(n_qtiles),
-                       scale_log2, op);
+    launch<64, 2>(items, stream, qp, knp, vnp, total_tokens, kp, vp, pool_slots, req_to_token, rtt_rows,
+                  rtt_stride, req_pool_idx, prefix_lens, extend_lens, extend_start, batch, hkv, grp, nq,
+                  scale_log2, op);
   }
   return ra_check_launch("ra_extend_attention");
 }
