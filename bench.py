@@ -96,6 +96,8 @@ def main():
     ap.add_argument("--workload", default="mixed")
     ap.add_argument("--cpu-budget", type=float, default=20.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration-mib", type=int, default=0,
+                    help="after the timed loop, run one device copy of this size (HBM counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for {args.gpus}); the path shards by request, "
@@ -178,6 +180,15 @@ def main():
               "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s"})
     if other["achieved"] is not None:
         other["frac"] = other["achieved"] / other["peak"]
+
+    if args.copy_calibration_mib:
+        n = args.copy_calibration_mib << 20
+        src = torch.empty(n, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"[bench] calibration copy: {n} bytes read, {n} bytes written")
 
     value = work["attended"] / (ms_step * 1e-3)
     line = {

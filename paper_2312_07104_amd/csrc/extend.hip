@@ -28,7 +28,7 @@
 // The DMAs are issued from inline assembly: the compiler would otherwise
 // wait for every outstanding DMA before each LDS read, serialising the
 // pipeline.  Waits are explicit s_waitcnt vmcnt at the top of each tile.
-#include <cstdlib>
+#include <type_traits>
 
 #include "device_common.h"
 
@@ -58,27 +58,31 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | 0x0F70);
 }
 
-template <int PIECES>
-__device__ __forceinline__ int swz(int row) {
-  return (row ^ ((row >> 4) << 2)) & (PIECES - 1);
-}
+// LDS tile layout (K and V alike): [piece group pg = D/32][key row 0..63]
+// [4 pieces of 16 B], i.e. each row's 2*D bytes are split into 64-byte
+// groups stored 4 KB apart.  One DMA instruction fills 16 rows of one piece
+// group (1 KB contiguous).  The 16-byte piece q of row r sits at physical
+// slot q ^ rot(r), rot(r) = bit 3 and bit 4 of r swapped into bits 1 and 0.
+// With this layout every MFMA operand read below is one per-lane offset
+// (fixed for the whole kernel) plus a compile-time immediate, and the 16
+// lanes of each LDS phase hit 16 distinct 16-byte bank groups.
+__device__ __forceinline__ int rot34(int r) { return (((r >> 3) & 1) << 1) | ((r >> 4) & 1); }
 
-template <int D, int NS>
-__global__ __launch_bounds__(256, NS == 2 ? 2 : 1) void extend_kernel(
+template <int D>
+__global__ __launch_bounds__(256, 2) void extend_kernel(
     const __bf16* __restrict__ q, const __bf16* __restrict__ k_new, const __bf16* __restrict__ v_new,
     int64_t total_tokens, const __bf16* __restrict__ k_pool, const __bf16* __restrict__ v_pool,
     int64_t pool_slots, const int32_t* __restrict__ rtt, int64_t rtt_rows, int64_t rtt_stride,
     const int32_t* __restrict__ req_pool_idx, const int32_t* __restrict__ prefix_lens,
     const int32_t* __restrict__ extend_lens, const int32_t* __restrict__ extend_start, int32_t batch,
     int32_t hkv, int32_t grp, int32_t n_qtiles, float scale_log2, __bf16* __restrict__ out) {
-  constexpr int KS = D / 32;                  // MFMA k-steps over the head dimension
+  constexpr int KS = D / 32;                  // MFMA k-steps over the head dimension = piece groups
   constexpr int DB = D / 16;                  // 16-row blocks of O^T
-  constexpr int PIECES = D / 8;               // 16-byte pieces per row
-  constexpr int ROWB = 2 * D;                 // bytes per K or V row
-  constexpr int TILE_B = kBN * ROWB;          // bytes per K (or V) tile
+  constexpr int GROUP_B = kBN * 64;           // bytes of one piece group of a tile
+  constexpr int TILE_B = KS * GROUP_B;        // bytes per K (or V) tile
   constexpr int LOADS = TILE_B / (256 * 16);  // DMA instructions per wave per tile per tensor
-  constexpr int RING = NS + 1;                // slot-index ring depth
-  __shared__ __align__(16) unsigned char kv_lds[NS][2][TILE_B];
+  constexpr int RING = 4;                     // slot-index ring depth
+  __shared__ __align__(16) unsigned char kv_lds[2][2][TILE_B];
   __shared__ __align__(16) int32_t idx_lds[RING][kBN];
 
   // Work-groups go to the 8 XCDs round-robin (block i -> XCD i % 8).  Items
@@ -117,51 +121,59 @@ __global__ __launch_bounds__(256, NS == 2 ? 2 : 1) void extend_kernel(
   const int c = lane & 15;
   const int g4 = lane >> 4;
 
-  // ---- DMA issue helpers ---------------------------------------------------
+  // ---- DMA lane mapping (fixed for the kernel) ----------------------------
+  // instruction ch = it*4 + wave covers row block rb = ch / KS, group pg = ch % KS
+  int dma_row[LOADS];
+  uint32_t dma_lds[LOADS];   // byte offset inside a tile (uniform per wave)
+  uint32_t dma_gofs[LOADS];  // byte offset inside the gathered global row
+#pragma unroll
+  for (int it = 0; it < LOADS; ++it) {
+    const int ch = it * 4 + wave;
+    const int rb = ch / KS, pg = ch % KS;
+    const int u = 16 * rb + (lane >> 2);
+    const int qlog = (lane & 3) ^ rot34(u);
+    dma_row[it] = u;
+    dma_lds[it] = pg * GROUP_B + rb * 1024;
+    dma_gofs[it] = static_cast<uint32_t>(g * D * 2 + 16 * (4 * pg + qlog));
+  }
+  const uint32_t row_bytes = static_cast<uint32_t>(hkv) * D * 2;
+  const unsigned char* kpool_b = reinterpret_cast<const unsigned char*>(k_pool);
+  const unsigned char* vpool_b = reinterpret_cast<const unsigned char*>(v_pool);
+  const unsigned char* knew_b = reinterpret_cast<const unsigned char*>(k_new);
+  const unsigned char* vnew_b = reinterpret_cast<const unsigned char*>(v_new);
+  const uint32_t smax = static_cast<uint32_t>(pool_slots - 1);
+
   auto issue_idx = [&](int tile) {  // wave 0 only: slot indices of one tile
     const int kb = tile * kBN;
     if (wave != 0 || tile >= n_tiles || kb >= P) return;
     const int pos = kb + lane;
     dma4(trow + (pos < P ? pos : 0), lds_addr(&idx_lds[tile % RING][0]));
   };
-  auto issue_kv = [&](int tile) {
+  auto issue_kv = [&](int tile, int stage) {
     if (tile >= n_tiles) return;
     const int kb = tile * kBN;
     const int32_t* ring = idx_lds[tile % RING];
-    unsigned char* kst = kv_lds[tile % NS][0];
-    unsigned char* vst = kv_lds[tile % NS][1];
+    const uint32_t kst = lds_addr(kv_lds[stage][0]);
+    const uint32_t vst = lds_addr(kv_lds[stage][1]);
 #pragma unroll
     for (int it = 0; it < LOADS; ++it) {
-      const int ch = it * 4 + wave;                // 1 KB chunk of the tile
-      const int u = (ch * 64 + lane) / PIECES;     // key row within the tile
-      const int pc = (lane % PIECES) ^ swz<PIECES>(u);
-      int pos = kb + u;
-      pos = pos < kend ? pos : kend - 1;           // padding rows repeat a real key
-      const __bf16* ks;
-      const __bf16* vs;
-      if (pos < P) {
-        int64_t s = ring[u];
-        s = (s >= 0 && s < pool_slots) ? s : 0;
-        const int64_t off = (s * hkv + g) * D + 8 * pc;
-        ks = k_pool + off;
-        vs = v_pool + off;
-      } else {
-        const int64_t off = ((start + pos - P) * hkv + g) * D + 8 * pc;
-        ks = k_new + off;
-        vs = v_new + off;
-      }
-      const uint32_t kb_lds = __builtin_amdgcn_readfirstlane(lds_addr(kst + ch * 1024));
-      const uint32_t vb_lds = __builtin_amdgcn_readfirstlane(lds_addr(vst + ch * 1024));
-      dma16(ks, kb_lds);
-      dma16(vs, vb_lds);
+      const int pos = min(kb + dma_row[it], kend - 1);  // padding rows repeat a real key
+      const bool pre = pos < P;
+      // the ring entry is only meaningful for prefix rows; reading it is always in bounds
+      const uint32_t slot = min(static_cast<uint32_t>(ring[dma_row[it]]), smax);  // negative -> huge -> clamped
+      const uint32_t row = pre ? slot : static_cast<uint32_t>(start + pos - P);
+      const uint64_t off = static_cast<uint64_t>(row) * row_bytes + dma_gofs[it];
+      dma16((pre ? kpool_b : knew_b) + off, __builtin_amdgcn_readfirstlane(kst + dma_lds[it]));
+      dma16((pre ? vpool_b : vnew_b) + off, __builtin_amdgcn_readfirstlane(vst + dma_lds[it]));
     }
   };
 
-  // ---- prologue: indices for the first NS tiles, K/V for the first NS-1 ---
-  for (int t = 0; t < NS; ++t) issue_idx(t);
+  // ---- prologue: indices for tiles 0 and 1, K/V for tile 0 ----------------
+  issue_idx(0);
+  issue_idx(1);
   wait_vmcnt<0>();
   __syncthreads();
-  for (int t = 0; t < NS - 1; ++t) issue_kv(t);
+  issue_kv(0, 0);
 
   // Q^T operands for the wave's two 16-query column blocks.
   bf16x8_t qT[2][KS];
@@ -181,74 +193,71 @@ __global__ __launch_bounds__(256, NS == 2 ? 2 : 1) void extend_kernel(
       qT[j][ks] = __builtin_bit_cast(bf16x8_t, qok[j] ? ld16(qp + 32 * ks) : make_uint4(0, 0, 0, 0));
   }
 
-  f32x4_t o[DB][2];
+  // O^T accumulators; block DB holds the row sums (A operand = ones), so the
+  // softmax denominator comes from the same bf16 P as the numerator.
+  f32x4_t o[DB + 1][2];
 #pragma unroll
-  for (int i = 0; i < DB; ++i) o[i][0] = o[i][1] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  float m_run[2] = {-INFINITY, -INFINITY};
-  float l_run[2] = {0.f, 0.f};
+  for (int i = 0; i <= DB; ++i) o[i][0] = o[i][1] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  float m_run[2] = {-INFINITY, -INFINITY};  // raw score units
+  const uint4 ones_w = make_uint4(0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u);
+  const bf16x8_t ones = __builtin_bit_cast(bf16x8_t, ones_w);
 
-  // Per-lane LDS offsets that do not depend on the tile.
-  // S^T block b of 32-key step k2 feeds A-operand row c with key
-  // 32 k2 + 8 (c >> 2) + 4 b + (c & 3).
-  int krow[2][2];
+  // Per-lane LDS offsets.  S^T block bb of 32-key step k2 feeds A-operand row
+  // c with key r = 32 k2 + 4 bb + r0, r0 = 8 (c >> 2) + (c & 3), so that the
+  // accumulator's row group g4 holds keys 8 g4 .. 8 g4 + 7 of the step:
+  // P^T's B-operand k slots in natural order.
+  const int r0 = 8 * (c >> 2) + (c & 3);
+  const uint32_t koff = r0 * 64 + 16 * (g4 ^ rot34(r0));
+  // V^T via transposed reads: lane supplies row 32 k2 + 4 h + (8 g4 + (c >> 2))
+  // and logical piece 2 db + ((c & 3) >> 1), half (c & 1).
+  uint32_t voff[2];
 #pragma unroll
-  for (int k2 = 0; k2 < 2; ++k2)
-#pragma unroll
-    for (int bb = 0; bb < 2; ++bb) krow[k2][bb] = 32 * k2 + 8 * (c >> 2) + 4 * bb + (c & 3);
+  for (int e = 0; e < 2; ++e)
+    voff[e] = (8 * g4 + (c >> 2)) * 64 + 16 * ((2 * e + ((c & 3) >> 1)) ^ rot34(8 * g4)) + 8 * (c & 1);
 
-  for (int t = 0; t < n_tiles; ++t) {
+  auto tile = [&](auto stage_tag, int t) {
+    constexpr int ST = decltype(stage_tag)::value;
     const int kbase = t * kBN;
-    if (NS == 2 || t + 1 >= n_tiles) {
-      wait_vmcnt<0>();
-    } else {
-      wait_vmcnt<2 * LOADS>();
-    }
+    wait_vmcnt<0>();
     __syncthreads();
-    issue_idx(t + NS);
-    issue_kv(t + NS - 1);
+    issue_idx(t + 2);
+    issue_kv(t + 1, ST ^ 1);
 
-    const unsigned char* kst = kv_lds[t % NS][0];
-    const unsigned char* vst = kv_lds[t % NS][1];
+    const unsigned char* kst = kv_lds[ST][0];
+    const unsigned char* vst = kv_lds[ST][1];
 
-    // S^T: key blocks (k2, bb) x query blocks j.
-    f32x4_t sacc[2][2][2];
+    f32x4_t sacc[2][2][2];  // [k2][bb][query block]
 #pragma unroll
-    for (int k2 = 0; k2 < 2; ++k2) {
+    for (int k2 = 0; k2 < 2; ++k2)
 #pragma unroll
       for (int bb = 0; bb < 2; ++bb) {
         sacc[k2][bb][0] = sacc[k2][bb][1] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-        const int r = krow[k2][bb];
-        const unsigned char* rp = kst + r * ROWB;
-        const int sw = swz<PIECES>(r);
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
-          const int pc = (4 * ks + g4) ^ sw;
-          const bf16x8_t a = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const uint4*>(rp + 16 * pc));
+          const bf16x8_t a = __builtin_bit_cast(
+              bf16x8_t, *reinterpret_cast<const uint4*>(kst + koff + ks * GROUP_B + (32 * k2 + 4 * bb) * 64));
           sacc[k2][bb][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qT[0][ks], sacc[k2][bb][0], 0, 0, 0);
           sacc[k2][bb][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qT[1][ks], sacc[k2][bb][1], 0, 0, 0);
         }
       }
-    }
-    // accumulator element (k2, bb, i) is key kbase + 32 k2 + 8 g4 + 4 bb + i.
-    // Online softmax in the base-2 domain with a lazily updated maximum: the
-    // running maximum (raw score units) only moves when some column's tile
-    // maximum exceeds it by more than 2^8 after scaling, so most tiles skip
-    // the rescale of O; exponentials stay <= 2^8, exact enough in fp32/bf16.
+    // Element (k2, bb, i) is key kbase + 32 k2 + 8 g4 + 4 bb + i.  Online
+    // softmax in the base-2 domain with a lazily moved maximum: it only moves
+    // when some column's tile maximum exceeds it by more than 2^8 after
+    // scaling, so most tiles skip the rescale; exponentials stay <= 2^8.
     const bool need_mask = kbase + kBN - 1 > P + tok0;
     bf16x8_t pT[2][2];  // [k2][query block]
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
-      float mt = -INFINITY;
       if (need_mask) {
 #pragma unroll
         for (int k2 = 0; k2 < 2; ++k2)
 #pragma unroll
           for (int bb = 0; bb < 2; ++bb)
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
+            for (int i = 0; i < 4; ++i)
               if (kbase + 32 * k2 + 8 * g4 + 4 * bb + i > qlim[j]) sacc[k2][bb][j][i] = -INFINITY;
-            }
       }
+      float mt = -INFINITY;
 #pragma unroll
       for (int k2 = 0; k2 < 2; ++k2)
 #pragma unroll
@@ -259,23 +268,18 @@ __global__ __launch_bounds__(256, NS == 2 ? 2 : 1) void extend_kernel(
       if (__builtin_amdgcn_ballot_w64((mt - m_run[j]) * scale_log2 > 8.f) != 0) {
         const float m_new = fmaxf(m_run[j], mt);
         const float alpha = ra_exp2((m_run[j] - m_new) * scale_log2);
-        l_run[j] *= alpha;
 #pragma unroll
-        for (int db = 0; db < DB; ++db) o[db][j] *= alpha;
+        for (int db = 0; db <= DB; ++db) o[db][j] *= alpha;
         m_run[j] = m_new;
       }
       const float mb = -m_run[j] * scale_log2;
-      float psum = 0.f;
 #pragma unroll
       for (int k2 = 0; k2 < 2; ++k2) {
         float p[8];
 #pragma unroll
         for (int bb = 0; bb < 2; ++bb)
 #pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            p[4 * bb + i] = ra_exp2(__builtin_fmaf(sacc[k2][bb][j][i], scale_log2, mb));
-            psum += p[4 * bb + i];
-          }
+          for (int i = 0; i < 4; ++i) p[4 * bb + i] = ra_exp2(__builtin_fmaf(sacc[k2][bb][j][i], scale_log2, mb));
         uint4 w;
         w.x = ra_pack_bf16x2(p[0], p[1]);
         w.y = ra_pack_bf16x2(p[2], p[3]);
@@ -283,46 +287,35 @@ __global__ __launch_bounds__(256, NS == 2 ? 2 : 1) void extend_kernel(
         w.w = ra_pack_bf16x2(p[6], p[7]);
         pT[k2][j] = __builtin_bit_cast(bf16x8_t, w);
       }
-      l_run[j] += psum;
     }
-    // O^T += V^T P^T.  Lane (c, g4) supplies row 32 k2 + 8 g4 + 4 h + (c >> 2),
-    // columns 16 db + 4 (c & 3) .. +3; it receives column 16 db + c of rows
-    // 32 k2 + 8 g4 + 4 h + 0..3.
+    // O^T += V^T P^T and the row sums += 1 P^T.
 #pragma unroll
     for (int k2 = 0; k2 < 2; ++k2) {
-      int voff[2];
-#pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        const int r = 32 * k2 + 8 * g4 + 4 * h + (c >> 2);
-        voff[h] = r * ROWB + 8 * ((c & 3) & 1);
-      }
 #pragma unroll
       for (int db = 0; db < DB; ++db) {
-        bf16x4_t lo, hi;
-        {
-          const int r = 32 * k2 + 8 * g4 + (c >> 2);
-          const int pc = (2 * db + ((c & 3) >> 1)) ^ swz<PIECES>(r);
-          lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
-              (__attribute__((address_space(3))) bf16x4_t*)(vst + voff[0] + 16 * pc));
-        }
-        {
-          const int r = 32 * k2 + 8 * g4 + 4 + (c >> 2);
-          const int pc = (2 * db + ((c & 3) >> 1)) ^ swz<PIECES>(r);
-          hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
-              (__attribute__((address_space(3))) bf16x4_t*)(vst + voff[1] + 16 * pc));
-        }
+        const unsigned char* vb = vst + voff[db & 1] + (db >> 1) * GROUP_B + 32 * k2 * 64;
+        const bf16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+            (__attribute__((address_space(3))) bf16x4_t*)(vb));
+        const bf16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+            (__attribute__((address_space(3))) bf16x4_t*)(vb + 4 * 64));
         const bf16x8_t a = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
         o[db][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pT[k2][0], o[db][0], 0, 0, 0);
         o[db][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pT[k2][1], o[db][1], 0, 0, 0);
       }
+      o[DB][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pT[k2][0], o[DB][0], 0, 0, 0);
+      o[DB][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pT[k2][1], o[DB][1], 0, 0, 0);
     }
+  };
+
+  for (int t = 0; t < n_tiles; t += 2) {
+    tile(std::integral_constant<int, 0>{}, t);
+    if (t + 1 < n_tiles) tile(std::integral_constant<int, 1>{}, t + 1);
   }
 
 #pragma unroll
   for (int j = 0; j < 2; ++j) {
-    const float l_tot = ra_sum_across_rows(l_run[j]);
     if (!qok[j]) continue;
-    const float inv = 1.f / l_tot;
+    const float inv = 1.f / o[DB][j][0];
     __bf16* op = out + qrow[j] * D + 4 * g4;
 #pragma unroll
     for (int db = 0; db < DB; ++db) {
@@ -334,13 +327,13 @@ __global__ __launch_bounds__(256, NS == 2 ? 2 : 1) void extend_kernel(
   }
 }
 
-template <int D, int NS>
+template <int D>
 void launch(int64_t items, hipStream_t stream, const __bf16* qp, const __bf16* knp, const __bf16* vnp,
             int64_t total_tokens, const __bf16* kp, const __bf16* vp, int64_t pool_slots, const int32_t* rtt,
             int64_t rtt_rows, int64_t rtt_stride, const int32_t* rpi, const int32_t* pl, const int32_t* el,
             const int32_t* es, int32_t batch, int32_t hkv, int32_t grp, int32_t n_qtiles, float scale_log2,
             __bf16* op) {
-  hipLaunchKernelGGL((extend_kernel<D, NS>), dim3(static_cast<uint32_t>(items)), dim3(256), 0, stream, qp, knp, vnp,
+  hipLaunchKernelGGL((extend_kernel<D>), dim3(static_cast<uint32_t>(items)), dim3(256), 0, stream, qp, knp, vnp,
                      total_tokens, kp, vp, pool_slots, rtt, rtt_rows, rtt_stride, rpi, pl, el, es, batch, hkv, grp,
                      n_qtiles, scale_log2, op);
 }
@@ -355,8 +348,8 @@ extern "C" int ra_extend_attention(const void* q, const void* k_new, const void*
                                    int32_t max_extend_len, int32_t hq, int32_t hkv, int32_t d, float scale,
                                    void* out, hipStream_t stream) {
   if (batch < 0 || hq <= 0 || hkv <= 0 || hq % hkv != 0 || (d != 64 && d != 128) || pool_slots <= 0 ||
-      rtt_rows <= 0 || rtt_stride <= 0 || max_extend_len < 0 || total_tokens < 0)
-    return ra_fail(RA_EINVAL, "ra_extend_attention: bad sizes");
+      rtt_rows <= 0 || rtt_stride <= 0 || max_extend_len < 0 || total_tokens < 0 || !(scale > 0.f))
+    return ra_fail(RA_EINVAL, "ra_extend_attention: bad sizes or scale");
   const int32_t grp = hq / hkv;
   if (grp != 1 && grp != 2 && grp != 4 && grp != 8 && grp != 16)
     return ra_fail(RA_EINVAL, "ra_extend_attention: Hq / Hkv must be 1, 2, 4, 8 or 16");
@@ -379,19 +372,12 @@ extern "C" int ra_extend_attention(const void* q, const void* k_new, const void*
   auto* vp = static_cast<const __bf16*>(v_pool);
   auto* op = static_cast<__bf16*>(out);
   const int32_t nq = static_cast<int32_t>(n_qtiles);
-  static const int ns_env = [] { const char* e = getenv("RA_EXTEND_NS"); return e ? atoi(e) : 2; }();
-  if (d == 128 && ns_env == 3) {
-    launch<128, 3>(items, stream, qp, knp, vnp, total_tokens, kp, vp, pool_slots, req_to_token, rtt_rows,
-                   rtt_stride, req_pool_idx, prefix_lens, extend_lens, extend_start, batch, hkv, grp, nq,
-                   scale_log2, op);
-  } else if (d == 128) {
-    launch<128, 2>(items, stream, qp, knp, vnp, total_tokens, kp, vp, pool_slots, req_to_token, rtt_rows,
-                   rtt_stride, req_pool_idx, prefix_lens, extend_lens, extend_start, batch, hkv, grp, nq,
-                   scale_log2, op);
+  if (d == 128) {
+    launch<128>(items, stream, qp, knp, vnp, total_tokens, kp, vp, pool_slots, req_to_token, rtt_rows, rtt_stride,
+                req_pool_idx, prefix_lens, extend_lens, extend_start, batch, hkv, grp, nq, scale_log2, op);
   } else {
-    launch<64, 2>(items, stream, qp, knp, vnp, total_tokens, kp, vp, pool_slots, req_to_token, rtt_rows,
-                  rtt_stride, req_pool_idx, prefix_lens, extend_lens, extend_start, batch, hkv, grp, nq,
-                  scale_log2, op);
+    launch<64>(items, stream, qp, knp, vnp, total_tokens, kp, vp, pool_slots, req_to_token, rtt_rows, rtt_stride,
+               req_pool_idx, prefix_lens, extend_lens, extend_start, batch, hkv, grp, nq, scale_log2, op);
   }
   return ra_check_launch("ra_extend_attention");
 }
