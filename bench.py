@@ -127,33 +127,44 @@ def main():
     out_e = torch.empty_like(inp.q_ext) if inp.n_ext else None
     out_d = torch.empty_like(inp.q_dec) if inp.n_dec else None
 
-    def step(ev=None):
-        if ev is not None:
-            ev[0].record(stream)
+    ws_t = workspace if ws_bytes else None
+
+    def step():
+        """One pass of the hot path: store new K/V, then the mixed batch call."""
         if n_new:
             pa.ra_store_kv(inp.new_slots, inp.k_new, inp.v_new, run.k_pool, run.v_pool)
-        if ev is not None:
-            ev[1].record(stream)
+        run.mixed(inp, workspace=ws_t, out_ext=out_e, out_dec=out_d)
+
+    def step_sequential(ev):
+        """The same work with each kernel timed alone (for the rooflines)."""
+        ev[0].record(stream)
+        if n_new:
+            pa.ra_store_kv(inp.new_slots, inp.k_new, inp.v_new, run.k_pool, run.v_pool)
+        ev[1].record(stream)
         if inp.n_ext:
             run.extend(inp, out=out_e)
-        if ev is not None:
-            ev[2].record(stream)
+        ev[2].record(stream)
         if inp.n_dec:
-            run.decode(inp, workspace=workspace, out=out_d)
-        if ev is not None:
-            ev[3].record(stream)
+            run.decode(inp, workspace=ws_t, out=out_d)
+        ev[3].record(stream)
 
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
-    torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
-        step(events[i])
+        step()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     ms_step = wall * 1e3 / args.steps
+
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    for i in range(args.steps):
+        step_sequential(events[i])
+    torch.cuda.synchronize()
+    ms_seq = (time.perf_counter() - t1) * 1e3 / args.steps
     t_store = float(np.mean([e[0].elapsed_time(e[1]) for e in events]))
     t_ext = float(np.mean([e[1].elapsed_time(e[2]) for e in events]))
     t_dec = float(np.mean([e[2].elapsed_time(e[3]) for e in events]))
@@ -201,6 +212,7 @@ def main():
                    "sum_extend_tokens": inp.total_ext, "sum_decode_context": work["sum_l"],
                    "history_requests": sc.history_len, "tree_calls": run.history_ops,
                    "hit_rate": inp.plan.hit_rate, "parallelism": "none (1 GPU)"},
+        "ms_per_step_sequential": ms_seq,
         "roofline": roof,
         "roofline_other": other,
         "kernels": kernels,

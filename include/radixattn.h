@@ -170,6 +170,28 @@ int ra_decode_attention(const void* q, const void* k_pool, const void* v_pool, i
 /* The chunk length (tokens) decode uses for these arguments. */
 int32_t ra_decode_chunk_len(int32_t batch, int32_t hkv, int32_t max_seq_len, int32_t num_splits);
 
+/* Mixed continuous batch (section 3: continuous batching merges new and
+ * running requests into one batch; Algorithm 1, B.merge and B.run): the
+ * extend requests and the decode requests of one batch in one call, over the
+ * same pool and slot table.  Arguments are those of ra_extend_attention
+ * (q_ext .. out_ext) and ra_decode_attention (q_dec .. out_dec).  The
+ * MFMA-bound extend runs on `stream`, the HBM-bound decode on a library-owned
+ * companion stream of the same device (default priority) that first waits
+ * for all work already queued on `stream`; `stream` then waits for the
+ * decode, so later work on `stream` sees both outputs.  No host
+ * synchronisation and no device allocation.  Either part may be empty
+ * (n_ext == 0 or n_dec == 0).  Not safe to call concurrently from several
+ * host threads on one device. */
+int ra_mixed_attention(const void* q_ext, const void* k_new, const void* v_new, int64_t total_tokens,
+                       const int32_t* req_pool_idx_ext, const int32_t* prefix_lens,
+                       const int32_t* extend_lens, const int32_t* extend_start, int32_t n_ext,
+                       int32_t max_extend_len, void* out_ext, const void* q_dec,
+                       const int32_t* req_pool_idx_dec, const int32_t* seq_lens, int32_t n_dec,
+                       int32_t max_seq_len, int32_t num_splits, void* workspace, size_t workspace_bytes,
+                       void* out_dec, const void* k_pool, const void* v_pool, int64_t pool_slots,
+                       const int32_t* req_to_token, int64_t rtt_rows, int64_t rtt_stride, int32_t hq,
+                       int32_t hkv, int32_t d, float scale, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -51,6 +51,9 @@ _SIGS = {
     "ra_decode_chunk_len": ([_i32, _i32, _i32, _i32], _i32),
     "ra_decode_attention": ([_vp, _vp, _vp, _i64, _vp, _i64, _i64, _vp, _vp, _i32, _i32, _i32, _i32, _i32,
                              ctypes.c_float, _i32, _vp, ctypes.c_size_t, _vp, _vp], ctypes.c_int),
+    "ra_mixed_attention": ([_vp, _vp, _vp, _i64, _vp, _vp, _vp, _vp, _i32, _i32, _vp,
+                            _vp, _vp, _vp, _i32, _i32, _i32, _vp, ctypes.c_size_t, _vp,
+                            _vp, _vp, _i64, _vp, _i64, _i64, _i32, _i32, _i32, ctypes.c_float, _vp], ctypes.c_int),
 }
 for _name, (_args, _res) in _SIGS.items():
     _f = getattr(_lib, _name)
@@ -253,3 +256,38 @@ def ra_decode_attention(q, k_pool, v_pool, req_to_token, req_pool_idx, seq_lens,
         _dev(seq_lens, torch.int32, "seq_lens"), b, int(max_seq_len), hq, hkv, d, float(scale), int(num_splits),
         ws_ptr, ws_bytes, _dev(out, torch.bfloat16, "out"), _stream(stream)))
     return out
+
+
+def ra_mixed_attention(q_ext, k_new, v_new, req_pool_idx_ext, prefix_lens, extend_lens, extend_start,
+                       max_extend_len: int, q_dec, req_pool_idx_dec, seq_lens, max_seq_len: int, k_pool, v_pool,
+                       req_to_token, scale: float, num_splits: int = 0, workspace=None, out_ext=None, out_dec=None,
+                       stream=None):
+    """One continuous batch: extend rows and decode rows over the same pool and
+    table; extend runs on the current stream, decode on the library's
+    companion stream, joined before the call's work completes on `stream`."""
+    import torch
+
+    total, hq, d = q_ext.shape
+    hkv = k_pool.shape[1]
+    n_ext, n_dec = prefix_lens.shape[0], q_dec.shape[0]
+    need = ra_decode_workspace_bytes(n_dec, hq, hkv, d, max_seq_len, num_splits)
+    if workspace is None and need:
+        workspace = torch.empty(need, dtype=torch.uint8, device=q_dec.device)
+    if out_ext is None:
+        out_ext = torch.empty_like(q_ext)
+    if out_dec is None:
+        out_dec = torch.empty_like(q_dec)
+    ws_ptr = _dev(workspace, None, "workspace") if workspace is not None else None
+    ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    _check(_lib.ra_mixed_attention(
+        _dev(q_ext, torch.bfloat16, "q_ext"), _dev(k_new, torch.bfloat16, "k_new"),
+        _dev(v_new, torch.bfloat16, "v_new"), total, _dev(req_pool_idx_ext, torch.int32, "req_pool_idx_ext"),
+        _dev(prefix_lens, torch.int32, "prefix_lens"), _dev(extend_lens, torch.int32, "extend_lens"),
+        _dev(extend_start, torch.int32, "extend_start"), n_ext, int(max_extend_len),
+        _dev(out_ext, torch.bfloat16, "out_ext"), _dev(q_dec, torch.bfloat16, "q_dec"),
+        _dev(req_pool_idx_dec, torch.int32, "req_pool_idx_dec"), _dev(seq_lens, torch.int32, "seq_lens"), n_dec,
+        int(max_seq_len), int(num_splits), ws_ptr, ws_bytes, _dev(out_dec, torch.bfloat16, "out_dec"),
+        _dev(k_pool, torch.bfloat16, "k_pool"), _dev(v_pool, torch.bfloat16, "v_pool"), k_pool.shape[0],
+        _dev(req_to_token, torch.int32, "req_to_token"), req_to_token.shape[0], req_to_token.shape[1], hq, hkv, d,
+        float(scale), _stream(stream)))
+    return out_ext, out_dec

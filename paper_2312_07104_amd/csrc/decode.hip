@@ -20,12 +20,13 @@
 // A chunk writes a normalised partial output and its log2-sum-exp; a second
 // kernel merges the chunks.  DMAs are issued from inline assembly (the
 // compiler would wait for them before every LDS read); waits are explicit.
+#include <cstdlib>
+
 #include "device_common.h"
 
 namespace {
 
-constexpr int kTile = 32;  // tokens per tile (two 16-row MFMA blocks)
-constexpr int kNS = 3;     // tiles in flight per wave
+constexpr int kTile = 32;  // tokens per tile of the default configuration (two 16-row MFMA blocks)
 
 __device__ __forceinline__ uint4 ld16(const __bf16* p) { return *reinterpret_cast<const uint4*>(p); }
 __device__ __forceinline__ uint32_t lds_addr(const void* p) {
@@ -42,33 +43,68 @@ __device__ __forceinline__ void wait_vmcnt() {
   static_assert(N >= 0 && N < 64, "vmcnt range");
   __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | 0x0F70);
 }
-template <int PIECES>
-__device__ __forceinline__ int swz(int row) {
-  return (row ^ ((row >> 4) << 2)) & (PIECES - 1);
+__device__ __forceinline__ int rot2(int x) { return ((x & 1) << 1) | ((x >> 1) & 1); }
+
+// LDS tile layout (K and V alike): [piece group pg = D/32][token row][4
+// pieces of 16 B]; the 16-byte piece q of row r sits at physical slot
+// q ^ sw(r), sw(r) = rot2 of bits [SH, SH+1] of r (SH = 3 for 32-row tiles,
+// 2 for 16-row tiles).  Every operand read is a per-lane offset fixed for the
+// kernel plus an immediate; each LDS phase touches 16 distinct bank groups.
+template <int TILE>
+__device__ __forceinline__ int tile_sw(int r) {
+  return rot2((r >> (TILE == 16 ? 2 : 3)) & 3);
 }
 
-template <int D>
+// Waits until the K/V tile t (and the slot indices issued with it) are in
+// LDS, given that `later` further K/V tiles (2*LOADS DMAs each) were issued
+// after it; vmcnt counts outstanding loads in issue order.
+template <int LOADS, int K>
+__device__ __forceinline__ void wait_for_tile_k(int later) {
+  if constexpr (K > 0) {
+    if (later >= K) {
+      wait_vmcnt<K * 2 * LOADS>();
+      return;
+    }
+    wait_for_tile_k<LOADS, K - 1>(later);
+  } else {
+    wait_vmcnt<0>();
+  }
+}
+template <int LOADS, int NS>
+__device__ __forceinline__ void wait_for_tile(int later) {
+  wait_for_tile_k<LOADS, NS - 2>(later);
+}
+
+template <int D, int TILE, int NS>
 __global__ __launch_bounds__(64) void decode_partial_kernel(
     const __bf16* __restrict__ q, const __bf16* __restrict__ k_pool, const __bf16* __restrict__ v_pool,
     int64_t pool_slots, const int32_t* __restrict__ rtt, int64_t rtt_rows, int64_t rtt_stride,
     const int32_t* __restrict__ req_pool_idx, const int32_t* __restrict__ seq_lens, int32_t batch,
     int32_t hkv, int32_t grp, int32_t chunk_len, int32_t max_splits, int32_t max_len, float scale_log2,
     float* __restrict__ ws_o, float* __restrict__ ws_lse, __bf16* __restrict__ out) {
-  constexpr int KS = D / 32;            // MFMA k-steps over the head dimension
-  constexpr int DB = D / 16;            // 16-row blocks of O^T
-  constexpr int PIECES = D / 8;         // 16-byte pieces per row
-  constexpr int ROWB = 2 * D;           // bytes per row
-  constexpr int TILE_B = kTile * ROWB;  // bytes per K (or V) tile
-  constexpr int LOADS = TILE_B / 1024;  // DMA instructions per tile per tensor
-  constexpr int RING = kNS + 1;
-  __shared__ __align__(16) unsigned char kv_lds[kNS][2][TILE_B];
+  static_assert(TILE == 16 || TILE == 32, "tile");
+  constexpr int KS = D / 32;             // MFMA k-steps over the head dimension = piece groups
+  constexpr int DB = D / 16;             // 16-row blocks of O^T
+  constexpr int GROUP_B = TILE * 64;     // bytes of one piece group of a tile
+  constexpr int TILE_B = KS * GROUP_B;   // bytes per K (or V) tile
+  constexpr int LOADS = TILE_B / 1024;   // DMA instructions per tile per tensor
+  constexpr int RING = 2 * NS;           // slot-index ring (indices run NS-1 tiles ahead of K/V)
+  constexpr int IDX_AHEAD = NS - 1;
+  __shared__ __align__(16) unsigned char kv_lds[NS][2][TILE_B];
   __shared__ __align__(16) int32_t idx_lds[RING][64];
 
-  const int item = blockIdx.x;
-  const int b = item % batch;
-  const int rest = item / batch;
-  const int g = rest % hkv;
-  const int split = rest / hkv;
+  // Work items ordered (kv head, split, request); each XCD (blocks go to the
+  // 8 XCDs round-robin) takes a contiguous eighth, so one XCD serves one kv
+  // head (with 8 kv heads) and the requests in flight on it share prefix
+  // chunks through its L2.
+  const int64_t n_items = static_cast<int64_t>(hkv) * max_splits * batch;
+  const int64_t per_xcd = (n_items + 7) / 8;
+  const int64_t item = static_cast<int64_t>(blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
+  if (item >= n_items) return;
+  const int g = static_cast<int>(item / (static_cast<int64_t>(max_splits) * batch));
+  const int rem = static_cast<int>(item % (static_cast<int64_t>(max_splits) * batch));
+  const int split = rem / batch;
+  const int b = rem % batch;
   const int L = min(seq_lens[b], max_len);  // host bound (<= rtt_stride, <= chunk_len * max_splits)
   if (L <= 0) return;
   const int n_splits = (L + chunk_len - 1) / chunk_len;
@@ -79,41 +115,49 @@ __global__ __launch_bounds__(64) void decode_partial_kernel(
   rrow = (rrow >= 0 && rrow < rtt_rows) ? rrow : 0;
   const int32_t* trow = rtt + rrow * rtt_stride;
   const int hq = hkv * grp;
-  const int n_tiles = (t_end - t_begin + kTile - 1) / kTile;
+  const int n_tiles = (t_end - t_begin + TILE - 1) / TILE;
 
   const int lane = threadIdx.x;
   const int c = lane & 15;   // query head column / A-operand row
   const int g4 = lane >> 4;  // which 16-lane row of the wave
 
+  // DMA lane mapping: instruction ch covers rows 16 (ch / KS) .. +15 of piece group ch % KS.
+  int dma_row[LOADS];
+  uint32_t dma_lds[LOADS], dma_gofs[LOADS];
+#pragma unroll
+  for (int ch = 0; ch < LOADS; ++ch) {
+    const int rb = ch / KS, pg = ch % KS;
+    const int u = 16 * rb + (lane >> 2);
+    dma_row[ch] = u;
+    dma_lds[ch] = pg * GROUP_B + rb * 1024;
+    dma_gofs[ch] = static_cast<uint32_t>(g * D * 2 + 16 * (4 * pg + ((lane & 3) ^ tile_sw<TILE>(u))));
+  }
+  const uint32_t row_bytes = static_cast<uint32_t>(hkv) * D * 2;
+  const unsigned char* kpool_b = reinterpret_cast<const unsigned char*>(k_pool);
+  const unsigned char* vpool_b = reinterpret_cast<const unsigned char*>(v_pool);
+  const uint32_t smax = static_cast<uint32_t>(pool_slots - 1);
+
   auto issue_idx = [&](int tile) {
     if (tile >= n_tiles) return;
-    int pos = t_begin + tile * kTile + (lane & 31);
-    pos = pos < t_end ? pos : t_end - 1;  // padding rows repeat a real token
+    const int pos = min(t_begin + tile * TILE + (lane & (TILE - 1)), t_end - 1);  // padding repeats a real token
     dma4(trow + pos, lds_addr(&idx_lds[tile % RING][0]));
   };
   auto issue_kv = [&](int tile) {
     if (tile >= n_tiles) return;
     const int32_t* ring = idx_lds[tile % RING];
-    unsigned char* kst = kv_lds[tile % kNS][0];
-    unsigned char* vst = kv_lds[tile % kNS][1];
+    const uint32_t kst = lds_addr(kv_lds[tile % NS][0]);
+    const uint32_t vst = lds_addr(kv_lds[tile % NS][1]);
 #pragma unroll
     for (int ch = 0; ch < LOADS; ++ch) {
-      const int u = (ch * 64 + lane) / PIECES;  // token row within the tile
-      const int pc = (lane % PIECES) ^ swz<PIECES>(u);
-      int64_t s = ring[u];
-      s = (s >= 0 && s < pool_slots) ? s : 0;
-      const int64_t off = (s * hkv + g) * D + 8 * pc;
-      dma16(k_pool + off, __builtin_amdgcn_readfirstlane(lds_addr(kst + ch * 1024)));
-      dma16(v_pool + off, __builtin_amdgcn_readfirstlane(lds_addr(vst + ch * 1024)));
+      const uint32_t slot = min(static_cast<uint32_t>(ring[dma_row[ch]]), smax);  // negative -> clamped
+      const uint64_t off = static_cast<uint64_t>(slot) * row_bytes + dma_gofs[ch];
+      dma16(kpool_b + off, __builtin_amdgcn_readfirstlane(kst + dma_lds[ch]));
+      dma16(vpool_b + off, __builtin_amdgcn_readfirstlane(vst + dma_lds[ch]));
     }
   };
 
-  // prologue: indices for kNS tiles, K/V for kNS - 1
-  for (int t = 0; t < kNS; ++t) issue_idx(t);
-  wait_vmcnt<0>();
-  __syncthreads();
-  for (int t = 0; t < kNS - 1; ++t) issue_kv(t);
-
+  // Q^T (loaded before the first DMA so that the compiler's wait for
+  // these loads does not also wait for the prologue's DMAs).
   // Q^T as the B operand: column c = head g*grp + c, k = 8*g4 .. of each step.
   bf16x8_t qt[KS];
   {
@@ -124,55 +168,66 @@ __global__ __launch_bounds__(64) void decode_partial_kernel(
       qt[ks] = __builtin_bit_cast(bf16x8_t, has ? ld16(qp + 32 * ks) : make_uint4(0, 0, 0, 0));
   }
 
+  // prologue: indices for the first NS-1+IDX_AHEAD tiles, K/V for the first NS-1
+  for (int t = 0; t < NS - 1 + IDX_AHEAD; ++t) issue_idx(t);
+  wait_vmcnt<0>();
+  __syncthreads();
+  for (int t = 0; t < NS - 1; ++t) issue_kv(t);
+
   f32x4_t o[DB];
 #pragma unroll
   for (int i = 0; i < DB; ++i) o[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   float m_run = -INFINITY;  // raw score units
   float l_run = 0.f;
-  // A-operand row c of S^T block bb is token 8 (c >> 2) + 4 bb + (c & 3), so
-  // that the accumulator's row group g4 holds tokens 8 g4 .. 8 g4 + 7: P^T's
-  // B-operand k slots in natural token order.
-  int krow[2];
+
+  // K A-operand rows: 32-row tiles feed row c of block bb with token
+  // 8 (c >> 2) + 4 bb + (c & 3), so accumulator row group g4 holds tokens
+  // 8 g4 .. 8 g4 + 7 (P^T's k slots in natural order); 16-row tiles feed
+  // token c and row group g4 holds tokens 4 g4 .. 4 g4 + 3.
+  const int kr0 = TILE == 32 ? 8 * (c >> 2) + (c & 3) : c;
+  const uint32_t koff = kr0 * 64 + 16 * (g4 ^ tile_sw<TILE>(kr0));
+  // V^T by transposed reads: lane supplies row vr0 (+ 4 h for 32-row tiles),
+  // logical piece 2 db + ((c & 3) >> 1), half (c & 1).
+  const int vr0 = TILE == 32 ? 8 * g4 + (c >> 2) : 4 * g4 + (c >> 2);
+  uint32_t voff[2];
 #pragma unroll
-  for (int bb = 0; bb < 2; ++bb) krow[bb] = 8 * (c >> 2) + 4 * bb + (c & 3);
+  for (int e = 0; e < 2; ++e)
+    voff[e] = vr0 * 64 + 16 * ((2 * e + ((c & 3) >> 1)) ^ tile_sw<TILE>(vr0)) + 8 * (c & 1);
+  constexpr int NB = TILE / 16;  // S^T blocks per tile
 
   for (int t = 0; t < n_tiles; ++t) {
-    if (t + 1 < n_tiles) {
-      wait_vmcnt<2 * LOADS>();  // tile t and the index tile t+kNS-1 have landed
-    } else {
-      wait_vmcnt<0>();
-    }
+    wait_for_tile<LOADS, NS>(min(NS - 2, n_tiles - 1 - t));
     __syncthreads();
-    issue_idx(t + kNS);
-    issue_kv(t + kNS - 1);
+    issue_idx(t + NS - 1 + IDX_AHEAD);
+    issue_kv(t + NS - 1);
 
-    const unsigned char* kst = kv_lds[t % kNS][0];
-    const unsigned char* vst = kv_lds[t % kNS][1];
-    const int t0 = t_begin + t * kTile;
+    const unsigned char* kst = kv_lds[t % NS][0];
+    const unsigned char* vst = kv_lds[t % NS][1];
+    const int t0 = t_begin + t * TILE;
 
-    f32x4_t sacc[2];
+    f32x4_t sacc[NB];
 #pragma unroll
-    for (int bb = 0; bb < 2; ++bb) {
+    for (int bb = 0; bb < NB; ++bb) {
       sacc[bb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-      const unsigned char* rp = kst + krow[bb] * ROWB;
-      const int sw = swz<PIECES>(krow[bb]);
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
-        const int pc = (4 * ks + g4) ^ sw;
-        const bf16x8_t a = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const uint4*>(rp + 16 * pc));
+        const bf16x8_t a = __builtin_bit_cast(
+            bf16x8_t, *reinterpret_cast<const uint4*>(kst + koff + ks * GROUP_B + 4 * bb * 64));
         sacc[bb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qt[ks], sacc[bb], 0, 0, 0);
       }
     }
-    // element (bb, i) is token t0 + 8 g4 + 4 bb + i
-    if (t0 + kTile > t_end) {
+    // element (bb, i) is token t0 + 8 g4 + 4 bb + i (32-row) or t0 + 4 g4 + i (16-row)
+    if (t0 + TILE > t_end) {
 #pragma unroll
-      for (int bb = 0; bb < 2; ++bb)
+      for (int bb = 0; bb < NB; ++bb)
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
-          if (t0 + 8 * g4 + 4 * bb + i >= t_end) sacc[bb][i] = -INFINITY;
+        for (int i = 0; i < 4; ++i) {
+          const int tok = TILE == 32 ? t0 + 8 * g4 + 4 * bb + i : t0 + 4 * g4 + i;
+          if (tok >= t_end) sacc[bb][i] = -INFINITY;
+        }
     }
-    float mt = fmaxf(fmaxf(fmaxf(sacc[0][0], sacc[0][1]), fmaxf(sacc[0][2], sacc[0][3])),
-                     fmaxf(fmaxf(sacc[1][0], sacc[1][1]), fmaxf(sacc[1][2], sacc[1][3])));
+    float mt = fmaxf(fmaxf(sacc[0][0], sacc[0][1]), fmaxf(sacc[0][2], sacc[0][3]));
+    if constexpr (NB == 2) mt = fmaxf(mt, fmaxf(fmaxf(sacc[1][0], sacc[1][1]), fmaxf(sacc[1][2], sacc[1][3])));
     mt = ra_max_across_rows(mt);
     if (__builtin_amdgcn_ballot_w64((mt - m_run) * scale_log2 > 8.f) != 0) {
       const float m_new = fmaxf(m_run, mt);
@@ -188,8 +243,12 @@ __global__ __launch_bounds__(64) void decode_partial_kernel(
     for (int bb = 0; bb < 2; ++bb)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        p[4 * bb + i] = ra_exp2(__builtin_fmaf(sacc[bb][i], scale_log2, mb));
-        l_run += p[4 * bb + i];
+        if (bb < NB) {
+          p[4 * bb + i] = ra_exp2(__builtin_fmaf(sacc[bb][i], scale_log2, mb));
+          l_run += p[4 * bb + i];
+        } else {
+          p[4 * bb + i] = 0.f;
+        }
       }
     uint4 pw;
     pw.x = ra_pack_bf16x2(p[0], p[1]);
@@ -198,20 +257,18 @@ __global__ __launch_bounds__(64) void decode_partial_kernel(
     pw.w = ra_pack_bf16x2(p[6], p[7]);
     const bf16x8_t pt = __builtin_bit_cast(bf16x8_t, pw);
 
-    // O^T += V^T P^T: lane (c, g4) supplies row 8 g4 + 4 h + (c >> 2),
-    // columns 16 db + 4 (c & 3) .. +3, and receives column 16 db + c of rows
-    // 8 g4 + 4 h + 0..3.
+    // O^T += V^T P^T: lane receives column 16 db + c of rows vr0 - (c >> 2) + 0..3 (+ 4 h).
 #pragma unroll
     for (int db = 0; db < DB; ++db) {
-      bf16x4_t half[2];
-#pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        const int r = 8 * g4 + 4 * h + (c >> 2);
-        const int pc = (2 * db + ((c & 3) >> 1)) ^ swz<PIECES>(r);
-        half[h] = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
-            (__attribute__((address_space(3))) bf16x4_t*)(vst + r * ROWB + 16 * pc + 8 * (c & 1)));
+      const unsigned char* vb = vst + voff[db & 1] + (db >> 1) * GROUP_B;
+      const bf16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((__attribute__((address_space(3))) bf16x4_t*)(vb));
+      bf16x4_t hi;
+      if constexpr (TILE == 32) {
+        hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((__attribute__((address_space(3))) bf16x4_t*)(vb + 4 * 64));
+      } else {
+        hi = __builtin_bit_cast(bf16x4_t, make_uint2(0, 0));
       }
-      const bf16x8_t a = __builtin_shufflevector(half[0], half[1], 0, 1, 2, 3, 4, 5, 6, 7);
+      const bf16x8_t a = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
       o[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pt, o[db], 0, 0, 0);
     }
   }
@@ -290,8 +347,8 @@ extern "C" int32_t ra_decode_chunk_len(int32_t batch, int32_t hkv, int32_t max_s
   }
   // Largest chunk that still gives enough work items to keep every CU
   // streaming (256 CUs, a few waves each, several rounds for balance).
-  const int64_t target = 4096;
-  for (int32_t c : {2048, 1024, 512}) {
+  static const int64_t target = [] { const char* e = getenv("RA_DECODE_TARGET"); return e ? atoll(e) : 4096; }();
+  for (int32_t c : {4096, 2048, 1024, 512}) {
     if (static_cast<int64_t>(batch) * hkv * ceil_div(max_seq_len, c) >= target) return c;
   }
   return 256;
@@ -306,17 +363,17 @@ extern "C" size_t ra_decode_workspace_bytes(int32_t batch, int32_t hq, int32_t h
   return static_cast<size_t>(batch) * hq * splits * (d + 1) * sizeof(float);
 }
 
-extern "C" int ra_decode_attention(const void* q, const void* k_pool, const void* v_pool, int64_t pool_slots,
-                                   const int32_t* req_to_token, int64_t rtt_rows, int64_t rtt_stride,
-                                   const int32_t* req_pool_idx, const int32_t* seq_lens, int32_t batch,
-                                   int32_t max_seq_len, int32_t hq, int32_t hkv, int32_t d, float scale,
-                                   int32_t num_splits, void* workspace, size_t workspace_bytes, void* out,
-                                   hipStream_t stream) {
+// Argument checks shared with ra_mixed_attention: RA_OK when the call may
+// launch (or has nothing to do), an error status otherwise.
+int ra_decode_validate(const void* q, const void* k_pool, const void* v_pool, int64_t pool_slots,
+                       const int32_t* req_to_token, int64_t rtt_rows, int64_t rtt_stride, const int32_t* req_pool_idx,
+                       const int32_t* seq_lens, int32_t batch, int32_t max_seq_len, int32_t hq, int32_t hkv, int32_t d,
+                       float scale, int32_t num_splits, const void* workspace, size_t workspace_bytes,
+                       const void* out) {
   if (batch < 0 || hq <= 0 || hkv <= 0 || hq % hkv != 0 || (d != 64 && d != 128) || pool_slots <= 0 ||
       rtt_stride <= 0 || rtt_rows <= 0 || num_splits < 0 || !(scale > 0.f))
     return ra_fail(RA_EINVAL, "ra_decode_attention: bad sizes or scale");
-  const int32_t grp = hq / hkv;
-  if (grp > 16) return ra_fail(RA_EINVAL, "ra_decode_attention: more than 16 query heads per kv head");
+  if (hq / hkv > 16) return ra_fail(RA_EINVAL, "ra_decode_attention: more than 16 query heads per kv head");
   if (batch == 0) return ra_ok();
   if (max_seq_len <= 0) max_seq_len = static_cast<int32_t>(std::min<int64_t>(rtt_stride, INT32_MAX));
   if (max_seq_len > rtt_stride) return ra_fail(RA_EINVAL, "ra_decode_attention: max_seq_len > rtt_stride");
@@ -330,8 +387,27 @@ extern "C" int ra_decode_attention(const void* q, const void* k_pool, const void
   if (workspace_bytes < need || (need && !workspace))
     return ra_fail(RA_EINVAL, "ra_decode_attention: workspace too small");
   if (need && !ra_aligned16(workspace)) return ra_fail(RA_EINVAL, "ra_decode_attention: workspace alignment");
+  if (static_cast<int64_t>(batch) * hkv * splits + 8 > INT32_MAX)
+    return ra_fail(RA_EINVAL, "ra_decode_attention: too many work items");
+  return ra_ok();
+}
+
+extern "C" int ra_decode_attention(const void* q, const void* k_pool, const void* v_pool, int64_t pool_slots,
+                                   const int32_t* req_to_token, int64_t rtt_rows, int64_t rtt_stride,
+                                   const int32_t* req_pool_idx, const int32_t* seq_lens, int32_t batch,
+                                   int32_t max_seq_len, int32_t hq, int32_t hkv, int32_t d, float scale,
+                                   int32_t num_splits, void* workspace, size_t workspace_bytes, void* out,
+                                   hipStream_t stream) {
+  const int st0 = ra_decode_validate(q, k_pool, v_pool, pool_slots, req_to_token, rtt_rows, rtt_stride, req_pool_idx,
+                                     seq_lens, batch, max_seq_len, hq, hkv, d, scale, num_splits, workspace,
+                                     workspace_bytes, out);
+  if (st0 != RA_OK || batch == 0) return st0;
+  if (max_seq_len <= 0) max_seq_len = static_cast<int32_t>(std::min<int64_t>(rtt_stride, INT32_MAX));
+  const int32_t grp = hq / hkv;
+  const int32_t chunk = ra_decode_chunk_len(batch, hkv, max_seq_len, num_splits);
+  const int64_t splits = ceil_div(max_seq_len, chunk);
+  const size_t need = ra_decode_workspace_bytes(batch, hq, hkv, d, max_seq_len, num_splits);
   const int64_t items = static_cast<int64_t>(batch) * hkv * splits;
-  if (items > INT32_MAX) return ra_fail(RA_EINVAL, "ra_decode_attention: too many work items");
   float* ws_o = static_cast<float*>(workspace);
   float* ws_lse = need ? ws_o + static_cast<int64_t>(batch) * hq * splits * d : nullptr;
   const float scale_log2 = scale * RA_LOG2E;
@@ -340,15 +416,24 @@ extern "C" int ra_decode_attention(const void* q, const void* k_pool, const void
   auto* kp = static_cast<const __bf16*>(k_pool);
   auto* vp = static_cast<const __bf16*>(v_pool);
   auto* op = static_cast<__bf16*>(out);
+  static const int variant = [] { const char* e = getenv("RA_DECODE_VARIANT"); return e ? atoi(e) : 0; }();
+  const int64_t grid = (items + 7) / 8 * 8;  // whole XCD rounds
+#define RA_LAUNCH_DECODE(DD, TT, NN)                                                                              \
+  hipLaunchKernelGGL((decode_partial_kernel<DD, TT, NN>), dim3(static_cast<uint32_t>(grid)), dim3(64), 0, stream, \
+                     qp, kp, vp, pool_slots, req_to_token, rtt_rows, rtt_stride, req_pool_idx, seq_lens, batch, hkv, \
+                     grp, chunk, max_splits, max_seq_len, scale_log2, ws_o, ws_lse, op)
   if (d == 128) {
-    hipLaunchKernelGGL(decode_partial_kernel<128>, dim3(static_cast<uint32_t>(items)), dim3(64), 0, stream, qp,
-                       kp, vp, pool_slots, req_to_token, rtt_rows, rtt_stride, req_pool_idx, seq_lens, batch, hkv,
-                       grp, chunk, max_splits, max_seq_len, scale_log2, ws_o, ws_lse, op);
+    switch (variant) {
+      case 1: RA_LAUNCH_DECODE(128, 32, 3); break;
+      case 2: RA_LAUNCH_DECODE(128, 16, 8); break;
+      case 3: RA_LAUNCH_DECODE(128, 16, 9); break;
+      case 4: RA_LAUNCH_DECODE(128, 16, 6); break;
+      default: RA_LAUNCH_DECODE(128, 32, 4); break;
+    }
   } else {
-    hipLaunchKernelGGL(decode_partial_kernel<64>, dim3(static_cast<uint32_t>(items)), dim3(64), 0, stream, qp,
-                       kp, vp, pool_slots, req_to_token, rtt_rows, rtt_stride, req_pool_idx, seq_lens, batch, hkv,
-                       grp, chunk, max_splits, max_seq_len, scale_log2, ws_o, ws_lse, op);
+    RA_LAUNCH_DECODE(64, 32, 3);
   }
+#undef RA_LAUNCH_DECODE
   int st = ra_check_launch("ra_decode_attention(partial)");
   if (st != RA_OK || splits <= 1) return st;
   const int64_t bh = static_cast<int64_t>(batch) * hq;

@@ -138,10 +138,25 @@ __global__ __launch_bounds__(256, 2) void extend_kernel(
   }
   const uint32_t row_bytes = static_cast<uint32_t>(hkv) * D * 2;
   const unsigned char* kpool_b = reinterpret_cast<const unsigned char*>(k_pool);
-  const unsigned char* vpool_b = reinterpret_cast<const unsigned char*>(v_pool);
   const unsigned char* knew_b = reinterpret_cast<const unsigned char*>(k_new);
-  const unsigned char* vnew_b = reinterpret_cast<const unsigned char*>(v_new);
+  // V rows sit at the same offsets from their own bases
+  const int64_t vpool_delta = reinterpret_cast<const unsigned char*>(v_pool) - kpool_b;
+  const int64_t vnew_delta = reinterpret_cast<const unsigned char*>(v_new) - knew_b;
   const uint32_t smax = static_cast<uint32_t>(pool_slots - 1);
+  // per-lane K source addresses of row 0 and per-wave LDS offsets, fixed for
+  // the kernel (integer addresses: the new-token base is rebased by -P rows)
+  uint64_t kpool_lane[LOADS], knew_lane[LOADS];
+  uint32_t lds_k[2][LOADS], lds_v[2][LOADS];
+#pragma unroll
+  for (int it = 0; it < LOADS; ++it) {
+    kpool_lane[it] = reinterpret_cast<uint64_t>(kpool_b) + dma_gofs[it];
+    knew_lane[it] = reinterpret_cast<uint64_t>(knew_b) + static_cast<uint64_t>(start - P) * row_bytes + dma_gofs[it];
+#pragma unroll
+    for (int st = 0; st < 2; ++st) {
+      lds_k[st][it] = __builtin_amdgcn_readfirstlane(lds_addr(kv_lds[st][0]) + dma_lds[it]);
+      lds_v[st][it] = __builtin_amdgcn_readfirstlane(lds_addr(kv_lds[st][1]) + dma_lds[it]);
+    }
+  }
 
   auto issue_idx = [&](int tile) {  // wave 0 only: slot indices of one tile
     const int kb = tile * kBN;
@@ -153,29 +168,38 @@ __global__ __launch_bounds__(256, 2) void extend_kernel(
     if (tile >= n_tiles) return;
     const int kb = tile * kBN;
     const int32_t* ring = idx_lds[tile % RING];
-    const uint32_t kst = lds_addr(kv_lds[stage][0]);
-    const uint32_t vst = lds_addr(kv_lds[stage][1]);
+    if (kb + kBN <= P) {
+      // every row of the tile is a cached prefix row: gather through the slots
 #pragma unroll
-    for (int it = 0; it < LOADS; ++it) {
-      const int pos = min(kb + dma_row[it], kend - 1);  // padding rows repeat a real key
-      const bool pre = pos < P;
-      // the ring entry is only meaningful for prefix rows; reading it is always in bounds
-      const uint32_t slot = min(static_cast<uint32_t>(ring[dma_row[it]]), smax);  // negative -> huge -> clamped
-      const uint32_t row = pre ? slot : static_cast<uint32_t>(start + pos - P);
-      const uint64_t off = static_cast<uint64_t>(row) * row_bytes + dma_gofs[it];
-      dma16((pre ? kpool_b : knew_b) + off, __builtin_amdgcn_readfirstlane(kst + dma_lds[it]));
-      dma16((pre ? vpool_b : vnew_b) + off, __builtin_amdgcn_readfirstlane(vst + dma_lds[it]));
+      for (int it = 0; it < LOADS; ++it) {
+        const uint32_t slot = min(static_cast<uint32_t>(ring[dma_row[it]]), smax);  // negative -> clamped
+        const uint64_t src = kpool_lane[it] + static_cast<uint64_t>(slot) * row_bytes;
+        dma16(reinterpret_cast<const void*>(src), lds_k[stage][it]);
+        dma16(reinterpret_cast<const void*>(src + vpool_delta), lds_v[stage][it]);
+      }
+    } else {
+#pragma unroll
+      for (int it = 0; it < LOADS; ++it) {
+        const int pos = min(kb + dma_row[it], kend - 1);  // padding rows repeat a real key
+        uint64_t src;
+        int64_t vdelta;
+        if (pos < P) {
+          const uint32_t slot = min(static_cast<uint32_t>(ring[dma_row[it]]), smax);
+          src = kpool_lane[it] + static_cast<uint64_t>(slot) * row_bytes;
+          vdelta = vpool_delta;
+        } else {
+          src = knew_lane[it] + static_cast<uint64_t>(pos) * row_bytes;
+          vdelta = vnew_delta;
+        }
+        dma16(reinterpret_cast<const void*>(src), lds_k[stage][it]);
+        dma16(reinterpret_cast<const void*>(src + vdelta), lds_v[stage][it]);
+      }
     }
   };
 
-  // ---- prologue: indices for tiles 0 and 1, K/V for tile 0 ----------------
-  issue_idx(0);
-  issue_idx(1);
-  wait_vmcnt<0>();
-  __syncthreads();
-  issue_kv(0, 0);
-
-  // Q^T operands for the wave's two 16-query column blocks.
+  // Q^T operands for the wave's two 16-query column blocks (loaded before
+  // the first DMA so that the compiler's wait for these loads does not also
+  // wait for the prologue's DMAs).
   bf16x8_t qT[2][KS];
   int qlim[2];  // last key position each of this lane's query columns may see
   bool qok[2];
@@ -192,6 +216,13 @@ __global__ __launch_bounds__(256, 2) void extend_kernel(
     for (int ks = 0; ks < KS; ++ks)
       qT[j][ks] = __builtin_bit_cast(bf16x8_t, qok[j] ? ld16(qp + 32 * ks) : make_uint4(0, 0, 0, 0));
   }
+
+  // ---- prologue: indices for tiles 0 and 1, K/V for tile 0 ----------------
+  issue_idx(0);
+  issue_idx(1);
+  wait_vmcnt<0>();
+  __syncthreads();
+  issue_kv(0, 0);
 
   // O^T accumulators; block DB holds the row sums (A operand = ones), so the
   // softmax denominator comes from the same bf16 P as the numerator.
@@ -340,13 +371,14 @@ void launch(int64_t items, hipStream_t stream, const __bf16* qp, const __bf16* k
 
 }  // namespace
 
-extern "C" int ra_extend_attention(const void* q, const void* k_new, const void* v_new, int64_t total_tokens,
-                                   const void* k_pool, const void* v_pool, int64_t pool_slots,
-                                   const int32_t* req_to_token, int64_t rtt_rows, int64_t rtt_stride,
-                                   const int32_t* req_pool_idx, const int32_t* prefix_lens,
-                                   const int32_t* extend_lens, const int32_t* extend_start, int32_t batch,
-                                   int32_t max_extend_len, int32_t hq, int32_t hkv, int32_t d, float scale,
-                                   void* out, hipStream_t stream) {
+// Argument checks shared with ra_mixed_attention: RA_OK when the call may
+// launch (or has nothing to do), an error status otherwise.
+int ra_extend_validate(const void* q, const void* k_new, const void* v_new, int64_t total_tokens,
+                       const void* k_pool, const void* v_pool, int64_t pool_slots, const int32_t* req_to_token,
+                       int64_t rtt_rows, int64_t rtt_stride, const int32_t* req_pool_idx,
+                       const int32_t* prefix_lens, const int32_t* extend_lens, const int32_t* extend_start,
+                       int32_t batch, int32_t max_extend_len, int32_t hq, int32_t hkv, int32_t d, float scale,
+                       void* out) {
   if (batch < 0 || hq <= 0 || hkv <= 0 || hq % hkv != 0 || (d != 64 && d != 128) || pool_slots <= 0 ||
       rtt_rows <= 0 || rtt_stride <= 0 || max_extend_len < 0 || total_tokens < 0 || !(scale > 0.f))
     return ra_fail(RA_EINVAL, "ra_extend_attention: bad sizes or scale");
@@ -360,6 +392,21 @@ extern "C" int ra_extend_attention(const void* q, const void* k_new, const void*
   if (!ra_aligned16(q) || !ra_aligned16(k_new) || !ra_aligned16(v_new) || !ra_aligned16(k_pool) ||
       !ra_aligned16(v_pool) || !ra_aligned16(out))
     return ra_fail(RA_EINVAL, "ra_extend_attention: pointers must be 16-byte aligned");
+  return ra_ok();
+}
+
+extern "C" int ra_extend_attention(const void* q, const void* k_new, const void* v_new, int64_t total_tokens,
+                                   const void* k_pool, const void* v_pool, int64_t pool_slots,
+                                   const int32_t* req_to_token, int64_t rtt_rows, int64_t rtt_stride,
+                                   const int32_t* req_pool_idx, const int32_t* prefix_lens,
+                                   const int32_t* extend_lens, const int32_t* extend_start, int32_t batch,
+                                   int32_t max_extend_len, int32_t hq, int32_t hkv, int32_t d, float scale,
+                                   void* out, hipStream_t stream) {
+  const int st = ra_extend_validate(q, k_new, v_new, total_tokens, k_pool, v_pool, pool_slots, req_to_token, rtt_rows,
+                                    rtt_stride, req_pool_idx, prefix_lens, extend_lens, extend_start, batch,
+                                    max_extend_len, hq, hkv, d, scale, out);
+  if (st != RA_OK || batch == 0 || max_extend_len == 0 || total_tokens == 0) return st;
+  const int32_t grp = hq / hkv;
   const int32_t tpb = kBM / grp;
   const int64_t n_qtiles = (static_cast<int64_t>(max_extend_len) + tpb - 1) / tpb;
   const int64_t items = (static_cast<int64_t>(batch) * hkv * n_qtiles + 7) / 8 * 8;  // whole XCD rounds

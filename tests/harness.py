@@ -161,6 +161,16 @@ class ScenarioRun:
             inp.q_dec, self.k_pool, self.v_pool, inp.table, inp.rpi[inp.n_ext:], inp.seq_lens, inp.max_seq_len,
             self.sc.scale, num_splits=num_splits, workspace=workspace, out=out)
 
+    def mixed(self, inp: PhaseInputs, num_splits: int = 0, workspace=None, out_ext=None, out_dec=None):
+        """Both halves of the batch in one ra_mixed_attention call."""
+        if inp.n_ext == 0 or inp.n_dec == 0:
+            return self.extend(inp, out=out_ext), self.decode(inp, num_splits, workspace, out_dec)
+        return pa.ra_mixed_attention(
+            inp.q_ext, inp.k_new[: inp.total_ext], inp.v_new[: inp.total_ext], inp.rpi[: inp.n_ext],
+            inp.prefix_lens, inp.extend_lens, inp.extend_start, inp.max_extend_len, inp.q_dec,
+            inp.rpi[inp.n_ext:], inp.seq_lens, inp.max_seq_len, self.k_pool, self.v_pool, inp.table, self.sc.scale,
+            num_splits=num_splits, workspace=workspace, out_ext=out_ext, out_dec=out_dec)
+
     def finish(self, idx: int, inp: PhaseInputs) -> None:
         ph = self.sc.phases[idx]
         ext = [(r.tokens, r.prefix_len, r.extend_len) for r in ph.extend]

@@ -215,3 +215,40 @@ def test_empty_and_invalid_arguments():
                                torch.zeros(1, dtype=torch.int32, device="cuda"),
                                torch.ones(1, dtype=torch.int32, device="cuda"),
                                torch.zeros(1, dtype=torch.int32, device="cuda"), 1, 0.125)
+
+
+def test_mixed_call_equals_separate_calls():
+    """ra_mixed_attention runs the same kernels on two streams: outputs are
+    bit-identical to separate calls, and ordered before later work on the
+    caller's stream."""
+    sc = S.cfg5_mixed_small()
+    log(f"case: mixed call seed={sc.seed}")
+    run = ScenarioRun(sc)
+    inp = run.prepare(0)
+    run.store(inp)
+    oe = run.extend(inp)
+    od = run.decode(inp)
+    torch.cuda.synchronize()
+    for rep in range(3):
+        me, md = run.mixed(inp)
+        s_e, s_d = me.float().sum(), md.float().sum()  # consumers queued on the caller's stream
+        torch.cuda.synchronize()
+        assert torch.equal(me, oe) and torch.equal(md, od)
+        assert torch.isfinite(s_e) and torch.isfinite(s_d)
+
+
+def test_mixed_call_rejects_bad_half_without_side_effects():
+    sc = S.cfg5_mixed_small()
+    log("case: mixed call argument error")
+    run = ScenarioRun(sc)
+    inp = run.prepare(0)
+    run.store(inp)
+    torch.cuda.synchronize()
+    out_d = torch.full_like(inp.q_dec, 7.0)
+    with pytest.raises(pa.RadixAttnError):
+        pa.ra_mixed_attention(inp.q_ext, inp.k_new[: inp.total_ext], inp.v_new[: inp.total_ext],
+                              inp.rpi[: inp.n_ext], inp.prefix_lens, inp.extend_lens, inp.extend_start,
+                              inp.max_extend_len, inp.q_dec, inp.rpi[inp.n_ext:], inp.seq_lens, inp.max_seq_len,
+                              run.k_pool, run.v_pool, inp.table, -1.0, out_dec=out_d)  # negative scale
+    torch.cuda.synchronize()
+    assert bool((out_d == 7.0).all())
