@@ -101,8 +101,9 @@ class RadixCache:
 
     def __del__(self):
         h = getattr(self, "_h", None)
-        if h:
-            _lib.ra_cache_destroy(h)
+        lib = _lib  # None once the interpreter is tearing the module down
+        if h and lib is not None:
+            lib.ra_cache_destroy(h)
             self._h = None
 
     def match_prefix(self, tokens):

@@ -26,6 +26,12 @@ HIP_ONLY = [f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang", "
             "-mno-amdgpu-ieee", "-fno-honor-nans"]
 
 
+# Per-source extra flags.  extend_wide.hip keeps its S^T MFMAs in VGPR form
+# (the softmax reads them with the VALU) although the kernel also uses AGPRs
+# for the O^T accumulators through inline assembly.
+EXTRA = {"extend_wide.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"]}
+
+
 def _run(cmd):
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
@@ -48,7 +54,7 @@ def build(verbose: bool = False) -> str:
         obj = os.path.join(BUILD, os.path.basename(src) + ".o")
         objs.append(obj)
         if src.endswith(".hip"):
-            cmds.append([HIPCC, *COMMON, *HIP_ONLY, "-c", src, "-o", obj])
+            cmds.append([HIPCC, *COMMON, *HIP_ONLY, *EXTRA.get(os.path.basename(src), []), "-c", src, "-o", obj])
         else:
             cmds.append([HIPCC, *COMMON, "-c", src, "-o", obj])
     with cf.ThreadPoolExecutor(max_workers=min(8, os.cpu_count() or 1)) as ex:

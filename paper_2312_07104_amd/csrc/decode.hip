@@ -9,7 +9,7 @@
 //     direct-to-LDS loads (global_load_lds_dwordx4), kNS tiles deep, no VGPR
 //     staging; the slot indices travel the same way one tile further ahead,
 //     so no load waits on an index.  Rows are unpadded (2*D bytes) with their
-//     16-byte pieces XOR-swizzled by swz(row) to spread LDS banks.
+//     16-byte pieces XOR-swizzled by ra_kv_swz(row) (conflict-free reads).
 //   * The G query heads that share the kv head are the N = 16 columns of
 //     bf16 MFMAs, so each K/V row fetched serves all G heads and the VALU is
 //     left for the softmax:  S^T[token, head] = K Q^T, O^T += V^T P^T, V^T
@@ -20,40 +20,17 @@
 // A chunk writes a normalised partial output and its log2-sum-exp; a second
 // kernel merges the chunks.  DMAs are issued from inline assembly (the
 // compiler would wait for them before every LDS read); waits are explicit.
-#include <cstdlib>
 
 #include "device_common.h"
+#include "lds_dma.h"
 
 namespace {
 
-constexpr int kTile = 32;  // tokens per tile of the default configuration (two 16-row MFMA blocks)
-
-__device__ __forceinline__ uint4 ld16(const __bf16* p) { return *reinterpret_cast<const uint4*>(p); }
-__device__ __forceinline__ uint32_t lds_addr(const void* p) {
-  return static_cast<uint32_t>(reinterpret_cast<uintptr_t>(p));
-}
-__device__ __forceinline__ void dma16(const void* g, uint32_t lds_base) {
-  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds_base) : "memory");
-}
-__device__ __forceinline__ void dma4(const void* g, uint32_t lds_base) {
-  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dword %0, off" ::"v"(g), "s"(lds_base) : "memory");
-}
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | 0x0F70);
-}
-__device__ __forceinline__ int rot2(int x) { return ((x & 1) << 1) | ((x >> 1) & 1); }
+constexpr int kTile = 32;  // tokens per tile (two 16-row MFMA blocks)
 
 // LDS tile layout (K and V alike): [piece group pg = D/32][token row][4
-// pieces of 16 B]; the 16-byte piece q of row r sits at physical slot
-// q ^ sw(r), sw(r) = rot2 of bits [SH, SH+1] of r (SH = 3 for 32-row tiles,
-// 2 for 16-row tiles).  Every operand read is a per-lane offset fixed for the
-// kernel plus an immediate; each LDS phase touches 16 distinct bank groups.
-template <int TILE>
-__device__ __forceinline__ int tile_sw(int r) {
-  return rot2((r >> (TILE == 16 ? 2 : 3)) & 3);
-}
+// pieces of 16 B], pieces swizzled by ra_kv_swz (conflict-free operand reads,
+// every read one per-lane offset plus an immediate).
 
 // Waits until the K/V tile t (and the slot indices issued with it) are in
 // LDS, given that `later` further K/V tiles (2*LOADS DMAs each) were issued
@@ -62,12 +39,12 @@ template <int LOADS, int K>
 __device__ __forceinline__ void wait_for_tile_k(int later) {
   if constexpr (K > 0) {
     if (later >= K) {
-      wait_vmcnt<K * 2 * LOADS>();
+      ra_wait_vmcnt<K * 2 * LOADS>();
       return;
     }
     wait_for_tile_k<LOADS, K - 1>(later);
   } else {
-    wait_vmcnt<0>();
+    ra_wait_vmcnt<0>();
   }
 }
 template <int LOADS, int NS>
@@ -75,14 +52,14 @@ __device__ __forceinline__ void wait_for_tile(int later) {
   wait_for_tile_k<LOADS, NS - 2>(later);
 }
 
-template <int D, int TILE, int NS>
+template <int D, int NS>
 __global__ __launch_bounds__(64) void decode_partial_kernel(
     const __bf16* __restrict__ q, const __bf16* __restrict__ k_pool, const __bf16* __restrict__ v_pool,
     int64_t pool_slots, const int32_t* __restrict__ rtt, int64_t rtt_rows, int64_t rtt_stride,
     const int32_t* __restrict__ req_pool_idx, const int32_t* __restrict__ seq_lens, int32_t batch,
     int32_t hkv, int32_t grp, int32_t chunk_len, int32_t max_splits, int32_t max_len, float scale_log2,
     float* __restrict__ ws_o, float* __restrict__ ws_lse, __bf16* __restrict__ out) {
-  static_assert(TILE == 16 || TILE == 32, "tile");
+  constexpr int TILE = kTile;
   constexpr int KS = D / 32;             // MFMA k-steps over the head dimension = piece groups
   constexpr int DB = D / 16;             // 16-row blocks of O^T
   constexpr int GROUP_B = TILE * 64;     // bytes of one piece group of a tile
@@ -130,7 +107,7 @@ __global__ __launch_bounds__(64) void decode_partial_kernel(
     const int u = 16 * rb + (lane >> 2);
     dma_row[ch] = u;
     dma_lds[ch] = pg * GROUP_B + rb * 1024;
-    dma_gofs[ch] = static_cast<uint32_t>(g * D * 2 + 16 * (4 * pg + ((lane & 3) ^ tile_sw<TILE>(u))));
+    dma_gofs[ch] = static_cast<uint32_t>(g * D * 2 + 16 * (4 * pg + ((lane & 3) ^ ra_kv_swz(u))));
   }
   const uint32_t row_bytes = static_cast<uint32_t>(hkv) * D * 2;
   const unsigned char* kpool_b = reinterpret_cast<const unsigned char*>(k_pool);
@@ -140,19 +117,19 @@ __global__ __launch_bounds__(64) void decode_partial_kernel(
   auto issue_idx = [&](int tile) {
     if (tile >= n_tiles) return;
     const int pos = min(t_begin + tile * TILE + (lane & (TILE - 1)), t_end - 1);  // padding repeats a real token
-    dma4(trow + pos, lds_addr(&idx_lds[tile % RING][0]));
+    ra_dma4(trow + pos, ra_lds_addr(&idx_lds[tile % RING][0]));
   };
   auto issue_kv = [&](int tile) {
     if (tile >= n_tiles) return;
     const int32_t* ring = idx_lds[tile % RING];
-    const uint32_t kst = lds_addr(kv_lds[tile % NS][0]);
-    const uint32_t vst = lds_addr(kv_lds[tile % NS][1]);
+    const uint32_t kst = ra_lds_addr(kv_lds[tile % NS][0]);
+    const uint32_t vst = ra_lds_addr(kv_lds[tile % NS][1]);
 #pragma unroll
     for (int ch = 0; ch < LOADS; ++ch) {
       const uint32_t slot = min(static_cast<uint32_t>(ring[dma_row[ch]]), smax);  // negative -> clamped
       const uint64_t off = static_cast<uint64_t>(slot) * row_bytes + dma_gofs[ch];
-      dma16(kpool_b + off, __builtin_amdgcn_readfirstlane(kst + dma_lds[ch]));
-      dma16(vpool_b + off, __builtin_amdgcn_readfirstlane(vst + dma_lds[ch]));
+      ra_dma16(kpool_b + off, __builtin_amdgcn_readfirstlane(kst + dma_lds[ch]));
+      ra_dma16(vpool_b + off, __builtin_amdgcn_readfirstlane(vst + dma_lds[ch]));
     }
   };
 
@@ -165,12 +142,12 @@ __global__ __launch_bounds__(64) void decode_partial_kernel(
     const __bf16* qp = q + (static_cast<int64_t>(b) * hq + g * grp + (has ? c : 0)) * D + 8 * g4;
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks)
-      qt[ks] = __builtin_bit_cast(bf16x8_t, has ? ld16(qp + 32 * ks) : make_uint4(0, 0, 0, 0));
+      qt[ks] = __builtin_bit_cast(bf16x8_t, has ? ra_ld16(qp + 32 * ks) : make_uint4(0, 0, 0, 0));
   }
 
   // prologue: indices for the first NS-1+IDX_AHEAD tiles, K/V for the first NS-1
   for (int t = 0; t < NS - 1 + IDX_AHEAD; ++t) issue_idx(t);
-  wait_vmcnt<0>();
+  ra_wait_vmcnt<0>();
   __syncthreads();
   for (int t = 0; t < NS - 1; ++t) issue_kv(t);
 
@@ -180,19 +157,17 @@ __global__ __launch_bounds__(64) void decode_partial_kernel(
   float m_run = -INFINITY;  // raw score units
   float l_run = 0.f;
 
-  // K A-operand rows: 32-row tiles feed row c of block bb with token
-  // 8 (c >> 2) + 4 bb + (c & 3), so accumulator row group g4 holds tokens
-  // 8 g4 .. 8 g4 + 7 (P^T's k slots in natural order); 16-row tiles feed
-  // token c and row group g4 holds tokens 4 g4 .. 4 g4 + 3.
-  const int kr0 = TILE == 32 ? 8 * (c >> 2) + (c & 3) : c;
-  const uint32_t koff = kr0 * 64 + 16 * (g4 ^ tile_sw<TILE>(kr0));
-  // V^T by transposed reads: lane supplies row vr0 (+ 4 h for 32-row tiles),
-  // logical piece 2 db + ((c & 3) >> 1), half (c & 1).
-  const int vr0 = TILE == 32 ? 8 * g4 + (c >> 2) : 4 * g4 + (c >> 2);
+  // K A-operand rows: row c of block bb gets token 8 (c >> 2) + 4 bb + (c & 3),
+  // so accumulator row group g4 holds tokens 8 g4 .. 8 g4 + 7 (P^T's k slots
+  // in natural order).
+  const int kr0 = 8 * (c >> 2) + (c & 3);
+  const uint32_t koff = kr0 * 64 + 16 * (g4 ^ ra_kv_swz(kr0));
+  // V^T by transposed reads: lane supplies row vr0 (+ 4 h), logical piece
+  // 2 db + ((c & 3) >> 1), half (c & 1).
+  const int vr0 = 8 * g4 + (c >> 2);
   uint32_t voff[2];
 #pragma unroll
-  for (int e = 0; e < 2; ++e)
-    voff[e] = vr0 * 64 + 16 * ((2 * e + ((c & 3) >> 1)) ^ tile_sw<TILE>(vr0)) + 8 * (c & 1);
+  for (int e = 0; e < 2; ++e) voff[e] = vr0 * 64 + 16 * ((2 * e + ((c & 3) >> 1)) ^ ra_kv_swz(vr0)) + 8 * (c & 1);
   constexpr int NB = TILE / 16;  // S^T blocks per tile
 
   for (int t = 0; t < n_tiles; ++t) {
@@ -216,18 +191,18 @@ __global__ __launch_bounds__(64) void decode_partial_kernel(
         sacc[bb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qt[ks], sacc[bb], 0, 0, 0);
       }
     }
-    // element (bb, i) is token t0 + 8 g4 + 4 bb + i (32-row) or t0 + 4 g4 + i (16-row)
+    // element (bb, i) is token t0 + 8 g4 + 4 bb + i
     if (t0 + TILE > t_end) {
 #pragma unroll
       for (int bb = 0; bb < NB; ++bb)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const int tok = TILE == 32 ? t0 + 8 * g4 + 4 * bb + i : t0 + 4 * g4 + i;
+          const int tok = t0 + 8 * g4 + 4 * bb + i;
           if (tok >= t_end) sacc[bb][i] = -INFINITY;
         }
     }
-    float mt = fmaxf(fmaxf(sacc[0][0], sacc[0][1]), fmaxf(sacc[0][2], sacc[0][3]));
-    if constexpr (NB == 2) mt = fmaxf(mt, fmaxf(fmaxf(sacc[1][0], sacc[1][1]), fmaxf(sacc[1][2], sacc[1][3])));
+    float mt = fmaxf(fmaxf(fmaxf(sacc[0][0], sacc[0][1]), fmaxf(sacc[0][2], sacc[0][3])),
+                     fmaxf(fmaxf(sacc[1][0], sacc[1][1]), fmaxf(sacc[1][2], sacc[1][3])));
     mt = ra_max_across_rows(mt);
     if (__builtin_amdgcn_ballot_w64((mt - m_run) * scale_log2 > 8.f) != 0) {
       const float m_new = fmaxf(m_run, mt);
@@ -240,15 +215,11 @@ __global__ __launch_bounds__(64) void decode_partial_kernel(
     const float mb = -m_run * scale_log2;
     float p[8];
 #pragma unroll
-    for (int bb = 0; bb < 2; ++bb)
+    for (int bb = 0; bb < NB; ++bb)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        if (bb < NB) {
-          p[4 * bb + i] = ra_exp2(__builtin_fmaf(sacc[bb][i], scale_log2, mb));
-          l_run += p[4 * bb + i];
-        } else {
-          p[4 * bb + i] = 0.f;
-        }
+        p[4 * bb + i] = ra_exp2(__builtin_fmaf(sacc[bb][i], scale_log2, mb));
+        l_run += p[4 * bb + i];
       }
     uint4 pw;
     pw.x = ra_pack_bf16x2(p[0], p[1]);
@@ -262,12 +233,8 @@ __global__ __launch_bounds__(64) void decode_partial_kernel(
     for (int db = 0; db < DB; ++db) {
       const unsigned char* vb = vst + voff[db & 1] + (db >> 1) * GROUP_B;
       const bf16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((__attribute__((address_space(3))) bf16x4_t*)(vb));
-      bf16x4_t hi;
-      if constexpr (TILE == 32) {
-        hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((__attribute__((address_space(3))) bf16x4_t*)(vb + 4 * 64));
-      } else {
-        hi = __builtin_bit_cast(bf16x4_t, make_uint2(0, 0));
-      }
+      const bf16x4_t hi =
+          __builtin_amdgcn_ds_read_tr16_b64_v4bf16((__attribute__((address_space(3))) bf16x4_t*)(vb + 4 * 64));
       const bf16x8_t a = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
       o[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pt, o[db], 0, 0, 0);
     }
@@ -347,9 +314,9 @@ extern "C" int32_t ra_decode_chunk_len(int32_t batch, int32_t hkv, int32_t max_s
   }
   // Largest chunk that still gives enough work items to keep every CU
   // streaming (256 CUs, a few waves each, several rounds for balance).
-  static const int64_t target = [] { const char* e = getenv("RA_DECODE_TARGET"); return e ? atoll(e) : 4096; }();
+  constexpr int64_t kTargetItems = 4096;
   for (int32_t c : {4096, 2048, 1024, 512}) {
-    if (static_cast<int64_t>(batch) * hkv * ceil_div(max_seq_len, c) >= target) return c;
+    if (static_cast<int64_t>(batch) * hkv * ceil_div(max_seq_len, c) >= kTargetItems) return c;
   }
   return 256;
 }
@@ -416,22 +383,17 @@ extern "C" int ra_decode_attention(const void* q, const void* k_pool, const void
   auto* kp = static_cast<const __bf16*>(k_pool);
   auto* vp = static_cast<const __bf16*>(v_pool);
   auto* op = static_cast<__bf16*>(out);
-  static const int variant = [] { const char* e = getenv("RA_DECODE_VARIANT"); return e ? atoi(e) : 0; }();
   const int64_t grid = (items + 7) / 8 * 8;  // whole XCD rounds
-#define RA_LAUNCH_DECODE(DD, TT, NN)                                                                              \
-  hipLaunchKernelGGL((decode_partial_kernel<DD, TT, NN>), dim3(static_cast<uint32_t>(grid)), dim3(64), 0, stream, \
+#define RA_LAUNCH_DECODE(DD, NN)                                                                                  \
+  hipLaunchKernelGGL((decode_partial_kernel<DD, NN>), dim3(static_cast<uint32_t>(grid)), dim3(64), 0, stream, \
                      qp, kp, vp, pool_slots, req_to_token, rtt_rows, rtt_stride, req_pool_idx, seq_lens, batch, hkv, \
                      grp, chunk, max_splits, max_seq_len, scale_log2, ws_o, ws_lse, op)
+  // 32-key tiles; four tiles in flight for D = 128 (32 KB of LDS per wave),
+  // three for D = 64.
   if (d == 128) {
-    switch (variant) {
-      case 1: RA_LAUNCH_DECODE(128, 32, 3); break;
-      case 2: RA_LAUNCH_DECODE(128, 16, 8); break;
-      case 3: RA_LAUNCH_DECODE(128, 16, 9); break;
-      case 4: RA_LAUNCH_DECODE(128, 16, 6); break;
-      default: RA_LAUNCH_DECODE(128, 32, 4); break;
-    }
+    RA_LAUNCH_DECODE(128, 4);
   } else {
-    RA_LAUNCH_DECODE(64, 32, 3);
+    RA_LAUNCH_DECODE(64, 3);
   }
 #undef RA_LAUNCH_DECODE
   int st = ra_check_launch("ra_decode_attention(partial)");

@@ -13,9 +13,9 @@
 //     through the request's slot-table row, new keys come from the contiguous
 //     k_new / v_new rows.  The slot indices themselves travel by DMA into a
 //     small LDS ring two tiles ahead, so a tile's gather never waits on its
-//     index load.  The K/V ring has NS stages.
+//     index load.  The K/V ring has two stages.
 //   * A DMA writes lane i's 16 bytes at base + 16 i, so rows sit unpadded at
-//     2*D bytes; the 16-byte pieces of row r are XOR-swizzled by swz(r) (the
+//     2*D bytes; the 16-byte pieces of row r are XOR-swizzled by ra_kv_swz(r) (the
 //     source address picks the piece) to spread LDS banks.
 //   * S^T[key, query] = K Q^T with the queries as the MFMA columns: each lane
 //     owns one query column, so the row max / row sum are in-lane plus two
@@ -31,42 +31,13 @@
 #include <type_traits>
 
 #include "device_common.h"
+#include "lds_dma.h"
 
 namespace {
 
 constexpr int kBM = 128;  // query rows per work-group
 constexpr int kBN = 64;   // keys per tile
-
-__device__ __forceinline__ uint4 ld16(const __bf16* p) { return *reinterpret_cast<const uint4*>(p); }
-
-__device__ __forceinline__ uint32_t lds_addr(const void* p) {
-  return static_cast<uint32_t>(reinterpret_cast<uintptr_t>(p));
-}
-
-// Direct global -> LDS copies: lane i's data lands at lds_base + size * i.
-__device__ __forceinline__ void dma16(const void* g, uint32_t lds_base) {
-  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds_base) : "memory");
-}
-__device__ __forceinline__ void dma4(const void* g, uint32_t lds_base) {
-  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dword %0, off" ::"v"(g), "s"(lds_base) : "memory");
-}
-
-// s_waitcnt vmcnt(n) with expcnt / lgkmcnt left unconstrained (gfx9 layout).
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | 0x0F70);
-}
-
-// LDS tile layout (K and V alike): [piece group pg = D/32][key row 0..63]
-// [4 pieces of 16 B], i.e. each row's 2*D bytes are split into 64-byte
-// groups stored 4 KB apart.  One DMA instruction fills 16 rows of one piece
-// group (1 KB contiguous).  The 16-byte piece q of row r sits at physical
-// slot q ^ rot(r), rot(r) = bit 3 and bit 4 of r swapped into bits 1 and 0.
-// With this layout every MFMA operand read below is one per-lane offset
-// (fixed for the whole kernel) plus a compile-time immediate, and the 16
-// lanes of each LDS phase hit 16 distinct 16-byte bank groups.
-__device__ __forceinline__ int rot34(int r) { return (((r >> 3) & 1) << 1) | ((r >> 4) & 1); }
+constexpr int64_t kWideMinRows = 256;  // query rows per kv head from which the 256-row kernel is used
 
 template <int D>
 __global__ __launch_bounds__(256, 2) void extend_kernel(
@@ -82,6 +53,11 @@ __global__ __launch_bounds__(256, 2) void extend_kernel(
   constexpr int TILE_B = KS * GROUP_B;        // bytes per K (or V) tile
   constexpr int LOADS = TILE_B / (256 * 16);  // DMA instructions per wave per tile per tensor
   constexpr int RING = 4;                     // slot-index ring depth
+  // A wave's DMA lane covers tile rows u0 + it * ROW_STEP (it < LOADS); the
+  // index ring stores row u at word LOADS * (u % ROW_STEP) + u / ROW_STEP so
+  // that a lane's LOADS slot indices are one vector LDS read.
+  constexpr int ROW_STEP = kBN / LOADS;
+  static_assert(LOADS == 2 || LOADS == 4, "index vector width");
   __shared__ __align__(16) unsigned char kv_lds[2][2][TILE_B];
   __shared__ __align__(16) int32_t idx_lds[RING][kBN];
 
@@ -131,7 +107,7 @@ __global__ __launch_bounds__(256, 2) void extend_kernel(
     const int ch = it * 4 + wave;
     const int rb = ch / KS, pg = ch % KS;
     const int u = 16 * rb + (lane >> 2);
-    const int qlog = (lane & 3) ^ rot34(u);
+    const int qlog = (lane & 3) ^ ra_kv_swz(u);
     dma_row[it] = u;
     dma_lds[it] = pg * GROUP_B + rb * 1024;
     dma_gofs[it] = static_cast<uint32_t>(g * D * 2 + 16 * (4 * pg + qlog));
@@ -153,29 +129,42 @@ __global__ __launch_bounds__(256, 2) void extend_kernel(
     knew_lane[it] = reinterpret_cast<uint64_t>(knew_b) + static_cast<uint64_t>(start - P) * row_bytes + dma_gofs[it];
 #pragma unroll
     for (int st = 0; st < 2; ++st) {
-      lds_k[st][it] = __builtin_amdgcn_readfirstlane(lds_addr(kv_lds[st][0]) + dma_lds[it]);
-      lds_v[st][it] = __builtin_amdgcn_readfirstlane(lds_addr(kv_lds[st][1]) + dma_lds[it]);
+      lds_k[st][it] = __builtin_amdgcn_readfirstlane(ra_lds_addr(kv_lds[st][0]) + dma_lds[it]);
+      lds_v[st][it] = __builtin_amdgcn_readfirstlane(ra_lds_addr(kv_lds[st][1]) + dma_lds[it]);
     }
   }
 
+  const int u0 = dma_row[0];  // = dma_row[it] - it * ROW_STEP
+  const int idx_pos = (lane % LOADS) * ROW_STEP + lane / LOADS;  // row whose slot lane's word holds
   auto issue_idx = [&](int tile) {  // wave 0 only: slot indices of one tile
     const int kb = tile * kBN;
     if (wave != 0 || tile >= n_tiles || kb >= P) return;
-    const int pos = kb + lane;
-    dma4(trow + (pos < P ? pos : 0), lds_addr(&idx_lds[tile % RING][0]));
+    const int pos = kb + idx_pos;
+    ra_dma4(trow + (pos < P ? pos : 0), ra_lds_addr(&idx_lds[tile % RING][0]));
+  };
+  auto read_slots = [&](int tile, int32_t (&sl)[LOADS]) {
+    const int32_t* w = &idx_lds[tile % RING][LOADS * u0];
+    if constexpr (LOADS == 4) {
+      const int4 v = *reinterpret_cast<const int4*>(w);
+      sl[0] = v.x, sl[1] = v.y, sl[2] = v.z, sl[3] = v.w;
+    } else {
+      const int2 v = *reinterpret_cast<const int2*>(w);
+      sl[0] = v.x, sl[1] = v.y;
+    }
   };
   auto issue_kv = [&](int tile, int stage) {
     if (tile >= n_tiles) return;
     const int kb = tile * kBN;
-    const int32_t* ring = idx_lds[tile % RING];
+    int32_t sl[LOADS];
+    if (kb < P) read_slots(tile, sl);
     if (kb + kBN <= P) {
       // every row of the tile is a cached prefix row: gather through the slots
 #pragma unroll
       for (int it = 0; it < LOADS; ++it) {
-        const uint32_t slot = min(static_cast<uint32_t>(ring[dma_row[it]]), smax);  // negative -> clamped
+        const uint32_t slot = min(static_cast<uint32_t>(sl[it]), smax);  // negative -> clamped
         const uint64_t src = kpool_lane[it] + static_cast<uint64_t>(slot) * row_bytes;
-        dma16(reinterpret_cast<const void*>(src), lds_k[stage][it]);
-        dma16(reinterpret_cast<const void*>(src + vpool_delta), lds_v[stage][it]);
+        ra_dma16(reinterpret_cast<const void*>(src), lds_k[stage][it]);
+        ra_dma16(reinterpret_cast<const void*>(src + vpool_delta), lds_v[stage][it]);
       }
     } else {
 #pragma unroll
@@ -184,15 +173,15 @@ __global__ __launch_bounds__(256, 2) void extend_kernel(
         uint64_t src;
         int64_t vdelta;
         if (pos < P) {
-          const uint32_t slot = min(static_cast<uint32_t>(ring[dma_row[it]]), smax);
+          const uint32_t slot = min(static_cast<uint32_t>(sl[it]), smax);
           src = kpool_lane[it] + static_cast<uint64_t>(slot) * row_bytes;
           vdelta = vpool_delta;
         } else {
           src = knew_lane[it] + static_cast<uint64_t>(pos) * row_bytes;
           vdelta = vnew_delta;
         }
-        dma16(reinterpret_cast<const void*>(src), lds_k[stage][it]);
-        dma16(reinterpret_cast<const void*>(src + vdelta), lds_v[stage][it]);
+        ra_dma16(reinterpret_cast<const void*>(src), lds_k[stage][it]);
+        ra_dma16(reinterpret_cast<const void*>(src + vdelta), lds_v[stage][it]);
       }
     }
   };
@@ -214,13 +203,13 @@ __global__ __launch_bounds__(256, 2) void extend_kernel(
     const __bf16* qp = q + qrow[j] * D + 8 * g4;
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks)
-      qT[j][ks] = __builtin_bit_cast(bf16x8_t, qok[j] ? ld16(qp + 32 * ks) : make_uint4(0, 0, 0, 0));
+      qT[j][ks] = __builtin_bit_cast(bf16x8_t, qok[j] ? ra_ld16(qp + 32 * ks) : make_uint4(0, 0, 0, 0));
   }
 
   // ---- prologue: indices for tiles 0 and 1, K/V for tile 0 ----------------
   issue_idx(0);
   issue_idx(1);
-  wait_vmcnt<0>();
+  ra_wait_vmcnt<0>();
   __syncthreads();
   issue_kv(0, 0);
 
@@ -238,18 +227,18 @@ __global__ __launch_bounds__(256, 2) void extend_kernel(
   // accumulator's row group g4 holds keys 8 g4 .. 8 g4 + 7 of the step:
   // P^T's B-operand k slots in natural order.
   const int r0 = 8 * (c >> 2) + (c & 3);
-  const uint32_t koff = r0 * 64 + 16 * (g4 ^ rot34(r0));
+  const uint32_t koff = r0 * 64 + 16 * (g4 ^ ra_kv_swz(r0));
   // V^T via transposed reads: lane supplies row 32 k2 + 4 h + (8 g4 + (c >> 2))
   // and logical piece 2 db + ((c & 3) >> 1), half (c & 1).
+  const int vr = 8 * g4 + (c >> 2);
   uint32_t voff[2];
 #pragma unroll
-  for (int e = 0; e < 2; ++e)
-    voff[e] = (8 * g4 + (c >> 2)) * 64 + 16 * ((2 * e + ((c & 3) >> 1)) ^ rot34(8 * g4)) + 8 * (c & 1);
+  for (int e = 0; e < 2; ++e) voff[e] = vr * 64 + 16 * ((2 * e + ((c & 3) >> 1)) ^ ra_kv_swz(vr)) + 8 * (c & 1);
 
   auto tile = [&](auto stage_tag, int t) {
     constexpr int ST = decltype(stage_tag)::value;
     const int kbase = t * kBN;
-    wait_vmcnt<0>();
+    ra_wait_vmcnt<0>();
     __syncthreads();
     issue_idx(t + 2);
     issue_kv(t + 1, ST ^ 1);
@@ -407,6 +396,13 @@ extern "C" int ra_extend_attention(const void* q, const void* k_new, const void*
                                     max_extend_len, hq, hkv, d, scale, out);
   if (st != RA_OK || batch == 0 || max_extend_len == 0 || total_tokens == 0) return st;
   const int32_t grp = hq / hkv;
+  // Requests with at least 256 query rows per kv head (new tokens x query
+  // heads per kv head) run on the 256-row kernel; shorter ones would leave
+  // most of its tile empty.
+  if (static_cast<int64_t>(max_extend_len) * grp >= kWideMinRows)
+    return ra_extend_wide_launch(q, k_new, v_new, total_tokens, k_pool, v_pool, pool_slots, req_to_token, rtt_rows,
+                                 rtt_stride, req_pool_idx, prefix_lens, extend_lens, extend_start, batch,
+                                 max_extend_len, hq, hkv, d, scale, out, stream);
   const int32_t tpb = kBM / grp;
   const int64_t n_qtiles = (static_cast<int64_t>(max_extend_len) + tpb - 1) / tpb;
   const int64_t items = (static_cast<int64_t>(batch) * hkv * n_qtiles + 7) / 8 * 8;  // whole XCD rounds

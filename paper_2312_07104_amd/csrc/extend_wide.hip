@@ -1,0 +1,462 @@
+// Extend attention with wide query tiles: the same operation as
+// ra_extend_attention's 128-row kernel (prefill of a request's new tokens over
+// its cached prefix, section 3 and Appendix A.1, plus causal attention among
+// the new tokens), organised for requests with many query rows.
+//
+// Work item = (request, kv head, query tile of 256 rows); one work-group of
+// eight waves per CU (two per SIMD, so one wave's MFMAs overlap the other's
+// softmax), each wave owning 32 query rows (two 16-column MFMA blocks).
+// Against the 128-row kernel (two work-groups of four waves per CU) every K/V
+// tile copied into LDS serves twice the queries, and the LDS holds a deeper
+// ring.
+//   * K/V tiles of 64 keys arrive by direct-to-LDS copies into a four-stage
+//     ring (two tiles of lead); the slot indices of a tile travel four tiles
+//     ahead into their own ring.  Rows use the ra_kv_swz piece layout.
+//   * Each 64-key tile is processed as two 32-key halves, software
+//     pipelined: the S^T = K Q^T MFMAs of half h+1 are issued in the same
+//     basic block as the softmax of half h, so the matrix cores run while the
+//     VALU computes exponentials.
+//   * O^T += V^T P^T accumulates in AGPRs (inline-assembly MFMAs with "a"
+//     operands); S^T stays in VGPRs, where the softmax reads it.  The
+//     compiler does not track hazards of inline assembly, so the code inserts
+//     the wait states itself: two after the VALU writes P^T, and a long
+//     s_nop sequence before the VALU touches O (rare rescale, epilogue).
+//   * Online softmax in the base-2 domain.  The running maximum moves only
+//     when some score exceeds it by more than 2^24 after exponentiation, so
+//     after the first half of a query tile the rescale path is practically
+//     never taken; the test is on each lane's partial maximum, so the common
+//     path has no cross-lane reduction.  Probabilities up to 2^24 cannot
+//     overflow the fp32 accumulators (2^24 times 2^22 keys times |v|).
+
+#include "device_common.h"
+#include "lds_dma.h"
+
+namespace {
+
+constexpr int kBM = 256;     // query rows per work-group
+constexpr int kBN = 64;      // keys per K/V tile
+constexpr int kStages = 4;   // K/V tiles resident in LDS
+constexpr int kRing = 4;     // slot-index ring (tiles)
+constexpr int kWaves = 8;    // waves per work-group
+constexpr int kQB = 2;       // 16-query column blocks per wave
+// exp2 argument ceiling of the lazy maximum: p <= 2^kLazyLog2
+constexpr float kLazyLog2 = 24.f;
+
+// O^T block += A B on AGPR accumulators (the compiler inserts no wait states
+// for it: callers keep VALU writes of A and B at least two wait states away).
+__device__ __forceinline__ void pv_mfma(f32x4_t& o, const bf16x8_t& a, const bf16x8_t& b) {
+  asm("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0" : "+a"(o) : "v"(a), "v"(b));
+}
+
+template <int D>
+__global__ __launch_bounds__(512, 1) void extend_wide_kernel(
+    const __bf16* __restrict__ q, const __bf16* __restrict__ k_new, const __bf16* __restrict__ v_new,
+    int64_t total_tokens, const __bf16* __restrict__ k_pool, const __bf16* __restrict__ v_pool,
+    int64_t pool_slots, const int32_t* __restrict__ rtt, int64_t rtt_rows, int64_t rtt_stride,
+    const int32_t* __restrict__ req_pool_idx, const int32_t* __restrict__ prefix_lens,
+    const int32_t* __restrict__ extend_lens, const int32_t* __restrict__ extend_start, int32_t batch,
+    int32_t hkv, int32_t grp, int32_t n_qtiles, float scale_log2, __bf16* __restrict__ out) {
+  constexpr int KS = D / 32;                  // MFMA k-steps over the head dimension = piece groups
+  constexpr int DB = D / 16;                  // 16-row blocks of O^T
+  constexpr int GROUP_B = kBN * 64;           // bytes of one piece group of a tile
+  constexpr int TILE_B = KS * GROUP_B;        // bytes per K (or V) tile
+  constexpr int STAGE_B = 2 * TILE_B;         // K tile then V tile
+  constexpr int LOADS = TILE_B / (kWaves * 64 * 16);  // DMA instructions per wave per tile per tensor
+  constexpr int ROW_STEP = kBN / LOADS;       // a DMA lane covers rows u0 + it * ROW_STEP
+  static_assert(LOADS == 1 || LOADS == 2, "index vector width");
+  __shared__ __align__(16) unsigned char kv_lds[kStages * STAGE_B];
+  __shared__ __align__(16) int32_t idx_lds[kRing][kBN];
+
+  // Work-groups go to the 8 XCDs round-robin (block i -> XCD i % 8); each XCD
+  // takes a contiguous eighth of the (kv head, request, query tile) order, so
+  // the work-groups on one XCD share K/V rows through its L2.
+  const int64_t n_items = static_cast<int64_t>(hkv) * batch * n_qtiles;
+  const int64_t per_xcd = (n_items + 7) / 8;
+  const int64_t item = static_cast<int64_t>(blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
+  if (item >= n_items) return;
+  const int g = static_cast<int>(item / (static_cast<int64_t>(batch) * n_qtiles));
+  const int rem = static_cast<int>(item % (static_cast<int64_t>(batch) * n_qtiles));
+  const int b = rem / n_qtiles;
+  const int qt = n_qtiles - 1 - rem % n_qtiles;
+  const int tpb = kBM / grp;  // new tokens per tile
+
+  const int64_t start = extend_start[b];
+  int64_t E = extend_lens[b];
+  if (start < 0 || start > total_tokens) return;
+  E = min(E, total_tokens - start);
+  const int tok0 = qt * tpb;
+  if (E <= 0 || tok0 >= E) return;
+  const int tok_end = static_cast<int>(min<int64_t>(E, tok0 + tpb));
+  const int P = static_cast<int>(min<int64_t>(max(prefix_lens[b], 0), rtt_stride));
+  int64_t rrow = req_pool_idx[b];
+  rrow = (rrow >= 0 && rrow < rtt_rows) ? rrow : 0;
+  const int32_t* trow = rtt + rrow * rtt_stride;
+  const int kend = P + tok_end;
+  const int hq = hkv * grp;
+  const int n_tiles = (kend + kBN - 1) / kBN;
+
+  const int tid = threadIdx.x;
+  const int wave = tid >> 6;
+  const int lane = tid & 63;
+  const int c = lane & 15;
+  const int g4 = lane >> 4;
+
+  // ---- DMA lane mapping (fixed for the kernel) ----------------------------
+  // instruction ch = it * kWaves + wave covers row block rb = ch / KS, group pg = ch % KS
+  int dma_row[LOADS];
+  uint32_t dma_lds[LOADS];   // byte offset inside a tile (uniform per wave)
+  uint32_t dma_gofs[LOADS];  // byte offset inside the gathered global row
+#pragma unroll
+  for (int it = 0; it < LOADS; ++it) {
+    const int ch = it * kWaves + wave;
+    const int rb = ch / KS, pg = ch % KS;
+    const int u = 16 * rb + (lane >> 2);
+    dma_row[it] = u;
+    dma_lds[it] = pg * GROUP_B + rb * 1024;
+    dma_gofs[it] = static_cast<uint32_t>(g * D * 2 + 16 * (4 * pg + ((lane & 3) ^ ra_kv_swz(u))));
+  }
+  const uint32_t row_bytes = static_cast<uint32_t>(hkv) * D * 2;
+  const unsigned char* kpool_b = reinterpret_cast<const unsigned char*>(k_pool);
+  const unsigned char* knew_b = reinterpret_cast<const unsigned char*>(k_new);
+  const int64_t vpool_delta = reinterpret_cast<const unsigned char*>(v_pool) - kpool_b;
+  const int64_t vnew_delta = reinterpret_cast<const unsigned char*>(v_new) - knew_b;
+  const uint32_t smax = static_cast<uint32_t>(pool_slots - 1);
+  uint64_t kpool_lane[LOADS], knew_lane[LOADS];
+#pragma unroll
+  for (int it = 0; it < LOADS; ++it) {
+    kpool_lane[it] = reinterpret_cast<uint64_t>(kpool_b) + dma_gofs[it];
+    knew_lane[it] = reinterpret_cast<uint64_t>(knew_b) + static_cast<uint64_t>(start - P) * row_bytes + dma_gofs[it];
+  }
+  const uint32_t lds_kv0 = ra_lds_addr(kv_lds);
+
+  // The index ring stores tile row u at word LOADS * (u % ROW_STEP) +
+  // u / ROW_STEP, so a lane's LOADS slot indices are one vector LDS read.
+  const int u0 = dma_row[0];
+  const int idx_pos = (lane % LOADS) * ROW_STEP + lane / LOADS;
+  // Wave 0 copies the slot indices of one tile.  It issues the copy for every
+  // tile (reading row position 0 where the tile has no cached rows) so that
+  // each wave's count of outstanding loads per tile is fixed.
+  auto issue_idx = [&](int tile) {
+    if (wave != 0) return;
+    const int pos = tile * kBN + idx_pos;
+    ra_dma4(trow + (tile < n_tiles && pos < P ? pos : 0), ra_lds_addr(&idx_lds[tile % kRing][0]));
+  };
+  // K and V rows of one tile into stage tile % kStages: 2 * LOADS copies per
+  // wave for every tile < n_tiles.
+  auto issue_kv = [&](int tile) {
+    if (tile >= n_tiles) return;
+    const int kb = tile * kBN;
+    const uint32_t kst = lds_kv0 + (tile % kStages) * STAGE_B;
+    int32_t sl[LOADS];
+    if (kb < P) {
+      const int32_t* w = &idx_lds[tile % kRing][LOADS * u0];
+      if constexpr (LOADS == 2) {
+        const int2 v = *reinterpret_cast<const int2*>(w);
+        sl[0] = v.x, sl[1] = v.y;
+      } else {
+        sl[0] = w[0];
+      }
+    }
+    if (kb + kBN <= P) {
+#pragma unroll
+      for (int it = 0; it < LOADS; ++it) {
+        const uint32_t slot = min(static_cast<uint32_t>(sl[it]), smax);  // negative -> clamped
+        const uint64_t src = kpool_lane[it] + static_cast<uint64_t>(slot) * row_bytes;
+        ra_dma16(reinterpret_cast<const void*>(src), kst + dma_lds[it]);
+        ra_dma16(reinterpret_cast<const void*>(src + vpool_delta), kst + TILE_B + dma_lds[it]);
+      }
+    } else {
+#pragma unroll
+      for (int it = 0; it < LOADS; ++it) {
+        const int pos = min(kb + dma_row[it], kend - 1);  // padding rows repeat a real key
+        uint64_t src;
+        int64_t vdelta;
+        if (pos < P) {
+          const uint32_t slot = min(static_cast<uint32_t>(sl[it]), smax);
+          src = kpool_lane[it] + static_cast<uint64_t>(slot) * row_bytes;
+          vdelta = vpool_delta;
+        } else {
+          src = knew_lane[it] + static_cast<uint64_t>(pos) * row_bytes;
+          vdelta = vnew_delta;
+        }
+        ra_dma16(reinterpret_cast<const void*>(src), kst + dma_lds[it]);
+        ra_dma16(reinterpret_cast<const void*>(src + vdelta), kst + TILE_B + dma_lds[it]);
+      }
+    }
+  };
+  // Top of tile u: K/V(u) and the indices needed next are in LDS for every
+  // wave, stage (u - 2) % kStages is free; refill it and extend the index
+  // ring.  Outstanding loads of this wave, oldest first: the group issued at
+  // the top of u - 2 (K/V(u), idx(u + 2)) and the group of u - 1
+  // (K/V(u + 1) if it exists, idx(u + 3)); the wait retires all but the
+  // latter.  Tile 0 follows the prologue, whose groups hold no index copy.
+  auto tile_top = [&](int u) {
+    const bool next = u + 1 < n_tiles;
+    if (u == 0 || wave != 0) {
+      if (next) ra_wait_vmcnt<2 * LOADS>(); else ra_wait_vmcnt<0>();
+    } else {
+      if (next) ra_wait_vmcnt<2 * LOADS + 1>(); else ra_wait_vmcnt<1>();
+    }
+    __syncthreads();
+    issue_kv(u + 2);
+    issue_idx(u + 4);
+  };
+
+  // Q^T operands of the wave's four 16-query column blocks.
+  bf16x8_t qT[kQB][KS];
+  int qlim[kQB];  // last key position each of this lane's query columns may see
+  bool qok[kQB];
+  int64_t qrow[kQB];
+#pragma unroll
+  for (int j = 0; j < kQB; ++j) {
+    const int m = 32 * wave + 16 * j + c;
+    const int it = tok0 + m / grp;
+    qok[j] = it < tok_end;
+    qlim[j] = P + min(it, tok_end - 1);
+    qrow[j] = (start + min(it, tok_end - 1)) * hq + g * grp + m % grp;
+    const __bf16* qp = q + qrow[j] * D + 8 * g4;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) qT[j][ks] = __builtin_bit_cast(bf16x8_t, ra_ld16(qp + 32 * ks));
+  }
+
+  // ---- prologue ------------------------------------------------------------
+#pragma unroll
+  for (int t = 0; t < kRing; ++t) issue_idx(t);
+  ra_wait_vmcnt<0>();
+  __syncthreads();
+  issue_kv(0);
+  issue_kv(1);
+
+  f32x4_t o[DB + 1][kQB];  // O^T blocks; block DB holds the row sums (A operand = ones)
+#pragma unroll
+  for (int i = 0; i <= DB; ++i)
+#pragma unroll
+    for (int j = 0; j < kQB; ++j) o[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  float m_run[kQB], thr[kQB], mb[kQB];  // running max (raw units), its lazy threshold, -m * scale_log2
+#pragma unroll
+  for (int j = 0; j < kQB; ++j) m_run[j] = thr[j] = -INFINITY, mb[j] = 0.f;
+  const float lazy_raw = kLazyLog2 / scale_log2;
+  // A operand of the row-sum MFMA.  It passes through the P^T wait-state asm
+  // below on every half, so the compiler cannot rematerialise it with a VALU
+  // move right in front of the MFMA.
+  bf16x8_t ones = __builtin_bit_cast(bf16x8_t, make_uint4(0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u));
+
+  // Per-lane LDS offsets.  S^T block bb of half k2 feeds A-operand row c with
+  // key r = 32 k2 + 4 bb + r0, r0 = 8 (c >> 2) + (c & 3): the accumulator's
+  // row group g4 then holds keys 8 g4 .. 8 g4 + 7 of the half, P^T's
+  // B-operand k slots in natural order.
+  const int r0 = 8 * (c >> 2) + (c & 3);
+  const uint32_t koff = r0 * 64 + 16 * (g4 ^ ra_kv_swz(r0));
+  // V^T via transposed reads: lane supplies row 32 k2 + 4 h + (8 g4 + (c >> 2))
+  // and logical piece 2 db + ((c & 3) >> 1), half (c & 1).
+  const int vr = 8 * g4 + (c >> 2);
+  uint32_t voff[2];
+#pragma unroll
+  for (int e = 0; e < 2; ++e) voff[e] = vr * 64 + 16 * ((2 * e + ((c & 3) >> 1)) ^ ra_kv_swz(vr)) + 8 * (c & 1);
+
+  // S^T of one 32-key half: s[bb][j], element i = key 32 k2 + 8 g4 + 4 bb + i.
+  // The S^T MFMAs run at raised wave priority, so the SIMD's arbiter issues
+  // them ahead of the other wave's softmax VALU work.
+  auto compute_s = [&](f32x4_t (&s)[2][kQB], int tile, int k2) {
+    __builtin_amdgcn_s_setprio(1);
+    const unsigned char* kst = kv_lds + (tile % kStages) * STAGE_B;
+#pragma unroll
+    for (int bb = 0; bb < 2; ++bb)
+#pragma unroll
+      for (int j = 0; j < kQB; ++j) s[bb][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+      for (int bb = 0; bb < 2; ++bb) {
+        const bf16x8_t a = __builtin_bit_cast(
+            bf16x8_t, *reinterpret_cast<const uint4*>(kst + koff + ks * GROUP_B + (32 * k2 + 4 * bb) * 64));
+#pragma unroll
+        for (int j = 0; j < kQB; ++j) s[bb][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qT[j][ks], s[bb][j], 0, 0, 0);
+      }
+    __builtin_amdgcn_s_setprio(0);
+  };
+
+  // Softmax of one half into P^T (bf16), then O^T += V^T P^T.
+  auto softmax_pv = [&](f32x4_t (&s)[2][kQB], int tile, int k2) {
+    const int kh = tile * kBN + 32 * k2;  // first key of the half
+    if (kh + 31 > P + tok0) {
+#pragma unroll
+      for (int j = 0; j < kQB; ++j)
+#pragma unroll
+        for (int bb = 0; bb < 2; ++bb)
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            if (kh + 8 * g4 + 4 * bb + i > qlim[j]) s[bb][j][i] = -INFINITY;
+    }
+    float mt[kQB];
+    bool up = false;
+#pragma unroll
+    for (int j = 0; j < kQB; ++j) {
+      mt[j] = fmaxf(fmaxf(fmaxf(s[0][j][0], s[0][j][1]), fmaxf(s[0][j][2], s[0][j][3])),
+                    fmaxf(fmaxf(s[1][j][0], s[1][j][1]), fmaxf(s[1][j][2], s[1][j][3])));
+      up |= mt[j] > thr[j];
+    }
+    if (__builtin_amdgcn_ballot_w64(up) != 0) {
+      // Rare: some column's maximum passed its threshold.  Move those
+      // columns' maxima and rescale their O^T.  The nops give the last
+      // MFMAs that wrote O time to retire before the VALU reads the AGPRs.
+#pragma unroll
+      for (int j = 0; j < kQB; ++j) {
+        const float mc = ra_max_across_rows(mt[j]);
+        float alpha = 1.f;
+        if (mc > thr[j]) {
+          alpha = ra_exp2((m_run[j] - mc) * scale_log2);  // 0 while m_run = -inf (O is still 0)
+          m_run[j] = mc;
+          thr[j] = mc + lazy_raw;
+          mb[j] = -mc * scale_log2;
+        }
+        if constexpr (DB == 8) {
+          asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 3"
+                       : "+a"(o[0][j]), "+a"(o[1][j]), "+a"(o[2][j]), "+a"(o[3][j]), "+a"(o[4][j]),
+                         "+a"(o[5][j]), "+a"(o[6][j]), "+a"(o[7][j]), "+a"(o[8][j]));
+        } else {
+          asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 3"
+                       : "+a"(o[0][j]), "+a"(o[1][j]), "+a"(o[2][j]), "+a"(o[3][j]), "+a"(o[4][j]));
+        }
+#pragma unroll
+        for (int db = 0; db <= DB; ++db) o[db][j] *= alpha;
+        // two wait states between the VALU writes of O and the next MFMA
+        if constexpr (DB == 8) {
+          asm volatile("s_nop 1"
+                       : "+a"(o[0][j]), "+a"(o[1][j]), "+a"(o[2][j]), "+a"(o[3][j]), "+a"(o[4][j]),
+                         "+a"(o[5][j]), "+a"(o[6][j]), "+a"(o[7][j]), "+a"(o[8][j]));
+        } else {
+          asm volatile("s_nop 1" : "+a"(o[0][j]), "+a"(o[1][j]), "+a"(o[2][j]), "+a"(o[3][j]), "+a"(o[4][j]));
+        }
+      }
+    }
+    bf16x8_t pT[kQB];
+#pragma unroll
+    for (int j = 0; j < kQB; ++j) {
+      float p[8];
+#pragma unroll
+      for (int bb = 0; bb < 2; ++bb)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) p[4 * bb + i] = ra_exp2(__builtin_fmaf(s[bb][j][i], scale_log2, mb[j]));
+      uint4 w;
+      w.x = ra_pack_bf16x2(p[0], p[1]);
+      w.y = ra_pack_bf16x2(p[2], p[3]);
+      w.z = ra_pack_bf16x2(p[4], p[5]);
+      w.w = ra_pack_bf16x2(p[6], p[7]);
+      pT[j] = __builtin_bit_cast(bf16x8_t, w);
+    }
+    // two wait states between the VALU writes of P^T and the MFMAs reading it
+    asm volatile("s_nop 1" : "+v"(pT[0]), "+v"(pT[1]), "+v"(ones));
+    const unsigned char* vst = kv_lds + (tile % kStages) * STAGE_B + TILE_B + 32 * k2 * 64;
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+      const unsigned char* vb = vst + voff[db & 1] + (db >> 1) * GROUP_B;
+      const bf16x4_t lo =
+          __builtin_amdgcn_ds_read_tr16_b64_v4bf16((__attribute__((address_space(3))) bf16x4_t*)(vb));
+      const bf16x4_t hi =
+          __builtin_amdgcn_ds_read_tr16_b64_v4bf16((__attribute__((address_space(3))) bf16x4_t*)(vb + 4 * 64));
+      const bf16x8_t a = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+#pragma unroll
+      for (int j = 0; j < kQB; ++j) pv_mfma(o[db][j], a, pT[j]);
+    }
+#pragma unroll
+    for (int j = 0; j < kQB; ++j) pv_mfma(o[DB][j], ones, pT[j]);
+  };
+
+  // ---- main loop: half h's softmax and PV run beside half h+1's S^T --------
+  // Ping-pong: waves 4..7 take each tile's barrier at the start of their
+  // iteration, waves 0..3 in its middle (the latest point before the S^T of
+  // the next tile).  The barrier aligns the two points, so the second group
+  // runs half an iteration behind the first and the two waves sharing a SIMD
+  // are in different phases (one in its softmax while the other issues MFMAs).
+  // Either point is after the wave's last read of the stage being refilled.
+  const bool lead = wave < kWaves / 2;
+  f32x4_t sa[2][kQB], sb[2][kQB];
+  tile_top(0);
+  compute_s(sa, 0, 0);
+  for (int t = 0; t < n_tiles; ++t) {
+    const bool more = t + 1 < n_tiles;
+    if (!lead && more) tile_top(t + 1);
+    compute_s(sb, t, 1);
+    softmax_pv(sa, t, 0);
+    if (more) {
+      if (lead) tile_top(t + 1);
+      compute_s(sa, t + 1, 0);
+    }
+    softmax_pv(sb, t, 1);
+  }
+
+  // No copy may still be landing in LDS once the work-group ends (the last
+  // index copies were issued past the final tile).
+  ra_wait_vmcnt<0>();
+  // Epilogue: let the last MFMAs retire, then normalise by the row sums.
+#pragma unroll
+  for (int j = 0; j < kQB; ++j) {
+    if constexpr (DB == 8) {
+      asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 3"
+                   : "+a"(o[0][j]), "+a"(o[1][j]), "+a"(o[2][j]), "+a"(o[3][j]), "+a"(o[4][j]), "+a"(o[5][j]),
+                     "+a"(o[6][j]), "+a"(o[7][j]), "+a"(o[8][j]));
+    } else {
+      asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 3"
+                   : "+a"(o[0][j]), "+a"(o[1][j]), "+a"(o[2][j]), "+a"(o[3][j]), "+a"(o[4][j]));
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < kQB; ++j) {
+    if (!qok[j]) continue;
+    const float inv = 1.f / o[DB][j][0];
+    __bf16* op = out + qrow[j] * D + 4 * g4;
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+      uint2 w;
+      w.x = ra_pack_bf16x2(o[db][j][0] * inv, o[db][j][1] * inv);
+      w.y = ra_pack_bf16x2(o[db][j][2] * inv, o[db][j][3] * inv);
+      *reinterpret_cast<uint2*>(op + 16 * db) = w;
+    }
+  }
+}
+
+template <int D>
+void launch_wide(int64_t items, hipStream_t stream, const __bf16* qp, const __bf16* knp, const __bf16* vnp,
+                 int64_t total_tokens, const __bf16* kp, const __bf16* vp, int64_t pool_slots, const int32_t* rtt,
+                 int64_t rtt_rows, int64_t rtt_stride, const int32_t* rpi, const int32_t* pl, const int32_t* el,
+                 const int32_t* es, int32_t batch, int32_t hkv, int32_t grp, int32_t n_qtiles, float scale_log2,
+                 __bf16* op) {
+  hipLaunchKernelGGL((extend_wide_kernel<D>), dim3(static_cast<uint32_t>(items)), dim3(kWaves * 64), 0, stream, qp, knp,
+                     vnp, total_tokens, kp, vp, pool_slots, rtt, rtt_rows, rtt_stride, rpi, pl, el, es, batch, hkv,
+                     grp, n_qtiles, scale_log2, op);
+}
+
+}  // namespace
+
+// Launches the wide-tile kernel for arguments ra_extend_validate accepted.
+int ra_extend_wide_launch(const void* q, const void* k_new, const void* v_new, int64_t total_tokens,
+                          const void* k_pool, const void* v_pool, int64_t pool_slots, const int32_t* req_to_token,
+                          int64_t rtt_rows, int64_t rtt_stride, const int32_t* req_pool_idx,
+                          const int32_t* prefix_lens, const int32_t* extend_lens, const int32_t* extend_start,
+                          int32_t batch, int32_t max_extend_len, int32_t hq, int32_t hkv, int32_t d, float scale,
+                          void* out, hipStream_t stream) {
+  const int32_t grp = hq / hkv;
+  const int32_t tpb = kBM / grp;
+  const int64_t n_qtiles = (static_cast<int64_t>(max_extend_len) + tpb - 1) / tpb;
+  const int64_t items = (static_cast<int64_t>(batch) * hkv * n_qtiles + 7) / 8 * 8;  // whole XCD rounds
+  if (items > INT32_MAX) return ra_fail(RA_EINVAL, "ra_extend_attention: too many work items");
+  const float scale_log2 = scale * RA_LOG2E;
+  auto* qp = static_cast<const __bf16*>(q);
+  auto* knp = static_cast<const __bf16*>(k_new);
+  auto* vnp = static_cast<const __bf16*>(v_new);
+  auto* kp = static_cast<const __bf16*>(k_pool);
+  auto* vp = static_cast<const __bf16*>(v_pool);
+  auto* op = static_cast<__bf16*>(out);
+  const int32_t nq = static_cast<int32_t>(n_qtiles);
+  if (d == 128) {
+    launch_wide<128>(items, stream, qp, knp, vnp, total_tokens, kp, vp, pool_slots, req_to_token, rtt_rows,
+                     rtt_stride, req_pool_idx, prefix_lens, extend_lens, extend_start, batch, hkv, grp, nq,
+                     scale_log2, op);
+  } else {
+    launch_wide<64>(items, stream, qp, knp, vnp, total_tokens, kp, vp, pool_slots, req_to_token, rtt_rows,
+                    rtt_stride, req_pool_idx, prefix_lens, extend_lens, extend_start, batch, hkv, grp, nq,
+                    scale_log2, op);
+  }
+  return ra_check_launch("ra_extend_attention(wide)");
+}

@@ -86,6 +86,33 @@ def test_ragged_extend_tiles(hq, hkv, d):
     _check_all(run, inp, oe, od, "ragged")
 
 
+@pytest.mark.parametrize("hq,hkv,d", [(8, 8, 64), (8, 8, 128), (16, 4, 128), (32, 8, 64)])
+def test_extend_kernels_agree_with_oracle(hq, hkv, d):
+    """The same batch through the 128-row kernel (query rows per kv head below
+    256) and through the 256-row kernel (forced by an inflated, still valid,
+    upper bound on the extend length): both match the oracle."""
+    log(f"case: both extend kernels hq={hq} hkv={hkv} d={d}")
+    grp = hq // hkv
+    e_max = max(1, 255 // grp)  # largest extend that stays on the 128-row kernel
+    ext = [(0, e_max), (70, max(1, e_max // 3)), (129, 1), (300, max(1, e_max - 5)), (64, 64 // grp or 1)]
+    sc = _scenario("two-kernels", hq, hkv, d, 4096, extend=ext, seed=31 + hq + d)
+    run = ScenarioRun(sc)
+    inp = run.prepare(0)
+    run.store(inp)
+    assert inp.max_extend_len * grp < 256
+    outs = {}
+    for name, bound in (("narrow", inp.max_extend_len), ("wide", max(inp.max_extend_len, 256 // grp + 1))):
+        outs[name] = pa.ra_extend_attention(
+            inp.q_ext, inp.k_new[: inp.total_ext], inp.v_new[: inp.total_ext], run.k_pool, run.v_pool, inp.table,
+            inp.rpi[: inp.n_ext], inp.prefix_lens, inp.extend_lens, inp.extend_start, bound, sc.scale)
+    torch.cuda.synchronize()
+    for name, o in outs.items():
+        got = _bf(o)
+        for toks, p, e, start in inp.ext_meta:
+            ref = oa.extend_reference(toks, p, e, sc.seed, sc.hq, sc.hkv, sc.d, sc.scale, sc.q_scale_pow2)
+            assert_close(got[start:start + e], ref, f"{name} kernel P={p} E={e}")
+
+
 @pytest.mark.parametrize("num_splits", [0, 1, 3, 16])
 def test_decode_boundaries(num_splits):
     lens = [1, 2, 31, 32, 33, 63, 64, 65, 255, 256, 257, 511, 512, 513, 1000, 2049]
