@@ -11,12 +11,19 @@ heads, 8 kv heads, head dim 128): 32 extend requests (cached prefix
 U[1024, 8192], extend U[256, 2048]) and 512 decode requests (context
 U[1024, 16384]) over a 4,194,304-slot pool, tables built by ~100k tree calls.
 
-Prints one JSON line.  Per-kernel durations come from HIP events recorded on
-the stream the kernels run on, inside the timed loop.
+Prints one JSON line.  The headline loop runs the steps back to back (the
+mixed call overlaps extend and decode on two streams).  A second loop runs the
+same work one kernel at a time, each step after a 1 GiB write that evicts L2
+and the Infinity Cache (cold caches), with HIP events recorded on the stream
+the kernels run on; its per-kernel durations give the rooflines.  HBM traffic
+per launch comes from rocprofv3 FETCH_SIZE / WRITE_SIZE passes stored in
+profiles/traffic.json, and is reported only while the kernel sources still
+hash to the values recorded there.
 """
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -29,6 +36,35 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
 BF16_PEAK_TFLOPS = 2500.0
+FLUSH_BYTES = 1 << 30
+CSRC = os.path.join(ROOT, "paper_2312_07104_amd", "csrc")
+# sources whose code a kernel's launch runs (traffic figures are tied to them)
+KERNEL_SOURCES = {
+    "extend": ["extend.hip", "extend_wide.hip", "lds_dma.h", "device_common.h"],
+    "decode": ["decode.hip", "lds_dma.h", "device_common.h"],
+}
+
+
+def sources_sha256(kernel):
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES[kernel]:
+        with open(os.path.join(CSRC, f), "rb") as fh:
+            h.update(f.encode() + b"\0" + fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic(kernel, workload):
+    """HBM bytes per launch from the committed counter summary, or None when
+    it is missing or was taken on different kernel sources."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    try:
+        with open(path) as fh:
+            rec = json.load(fh).get(f"{kernel}/{workload}")
+    except (OSError, ValueError):
+        return None
+    if not rec or rec.get("sources_sha256") != sources_sha256(kernel):
+        return None
+    return rec.get("hbm_bytes_per_launch")
 
 
 def log(*a):
@@ -128,6 +164,7 @@ def main():
     out_d = torch.empty_like(inp.q_dec) if inp.n_dec else None
 
     ws_t = workspace if ws_bytes else None
+    flush_buf = torch.empty(FLUSH_BYTES, dtype=torch.uint8, device="cuda")
 
     def step():
         """One pass of the hot path: store new K/V, then the mixed batch call."""
@@ -160,37 +197,41 @@ def main():
 
     events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
     torch.cuda.synchronize()
-    t1 = time.perf_counter()
     for i in range(args.steps):
+        flush_buf.fill_(i & 0xFF)  # cold L2 / Infinity Cache for the timed kernels
         step_sequential(events[i])
     torch.cuda.synchronize()
-    ms_seq = (time.perf_counter() - t1) * 1e3 / args.steps
+    ms_seq = float(np.mean([e[0].elapsed_time(e[3]) for e in events]))
     t_store = float(np.mean([e[0].elapsed_time(e[1]) for e in events]))
     t_ext = float(np.mean([e[1].elapsed_time(e[2]) for e in events]))
     t_dec = float(np.mean([e[2].elapsed_time(e[3]) for e in events]))
 
     kernels = {
         "store_kv": {"ms": t_store, "tokens": int(n_new)},
-        "extend": {"ms": t_ext, "tflops": work["ext_flops"] / (t_ext * 1e-3) / 1e12 if t_ext else None,
-                   "flops": work["ext_flops"]},
-        "decode": {"ms": t_dec, "gbs": work["dec_bytes"] / (t_dec * 1e-3) / 1e9 if t_dec else None,
-                   "bytes": work["dec_bytes"]},
+        "extend": {"ms": t_ext, "tflops": work["ext_flops"] / (t_ext * 1e-3) / 1e12,
+                   "flops": work["ext_flops"]} if inp.n_ext else None,
+        "decode": {"ms": t_dec, "gbs": work["dec_bytes"] / (t_dec * 1e-3) / 1e9,
+                   "bytes": work["dec_bytes"]} if inp.n_dec else None,
     }
     if inp.n_ext and t_ext >= t_dec:
         ach = work["ext_flops"] / (t_ext * 1e-3) / 1e12
         roof = {"kernel": "extend", "bound": "mfma", "achieved": ach, "peak": BF16_PEAK_TFLOPS,
-                "unit": "TFLOP/s", "frac": ach / BF16_PEAK_TFLOPS, "traffic": None}
+                "unit": "TFLOP/s", "frac": ach / BF16_PEAK_TFLOPS, "traffic": measured_traffic("extend", sc.name)}
     else:
         ach = work["dec_bytes"] / (t_dec * 1e-3) / 1e9
         roof = {"kernel": "decode", "bound": "hbm", "achieved": ach, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": ach / HBM_PEAK_GBS, "traffic": None}
-    # second roofline line for the other kernel, same definitions
-    other = ({"kernel": "decode", "bound": "hbm", "achieved": kernels["decode"]["gbs"], "peak": HBM_PEAK_GBS,
-              "unit": "GB/s"} if roof["kernel"] == "extend" else
-             {"kernel": "extend", "bound": "mfma", "achieved": kernels["extend"]["tflops"],
-              "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s"})
-    if other["achieved"] is not None:
+                "frac": ach / HBM_PEAK_GBS, "traffic": measured_traffic("decode", sc.name)}
+    # second roofline line for the other kernel (if the batch has it), same definitions
+    other = None
+    if roof["kernel"] == "extend" and kernels["decode"]:
+        other = {"kernel": "decode", "bound": "hbm", "achieved": kernels["decode"]["gbs"], "peak": HBM_PEAK_GBS,
+                 "unit": "GB/s"}
+    elif roof["kernel"] == "decode" and kernels["extend"]:
+        other = {"kernel": "extend", "bound": "mfma", "achieved": kernels["extend"]["tflops"],
+                 "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s"}
+    if other:
         other["frac"] = other["achieved"] / other["peak"]
+        other["traffic"] = measured_traffic(other["kernel"], sc.name)
 
     if args.copy_calibration_mib:
         n = args.copy_calibration_mib << 20
@@ -212,7 +253,7 @@ def main():
                    "sum_extend_tokens": inp.total_ext, "sum_decode_context": work["sum_l"],
                    "history_requests": sc.history_len, "tree_calls": run.history_ops,
                    "hit_rate": inp.plan.hit_rate, "parallelism": "none (1 GPU)"},
-        "ms_per_step_sequential": ms_seq,
+        "ms_per_step_sequential_cold": ms_seq,
         "roofline": roof,
         "roofline_other": other,
         "kernels": kernels,
