@@ -124,6 +124,37 @@ def cpu_baseline(sc, inp, budget_s: float):
                       f"({done_tokens} context tokens, {dt:.1f} s, inputs regenerated inside the timing)"}
 
 
+def scheduler_report(sc, n: int = 300):
+    """Theorem 3.1 on the workload's own request stream: the first n history
+    requests as one offline batch, cache = the longest of them, processed in
+    longest-shared-prefix-first, submission and random order; computed tokens
+    against the sum of the batch's radix-tree edge lengths."""
+    from paper_2312_07104_amd.runtime import run_offline
+
+    seqs = [np.asarray(sc.history(i), dtype=np.int32) for i in range(min(n, sc.history_len))]
+    if not seqs:
+        return None
+    root: dict = {}
+    edges = 0  # distinct non-empty prefixes = trie nodes below the root
+    for s in seqs:
+        node = root
+        for t in s.tolist():
+            nxt = node.get(t)
+            if nxt is None:
+                nxt = node[t] = {}
+                edges += 1
+            node = nxt
+    pool = max(len(s) for s in seqs)
+    out = {"requests": len(seqs), "prefill_tokens": int(sum(len(s) for s in seqs)), "edge_tokens": edges,
+           "cache_slots": pool}
+    t0 = time.perf_counter()
+    for policy in ("lspf", "fcfs", "random"):
+        r = run_offline(seqs, pool, policy, seed=1)
+        out[policy] = {"computed_tokens": r.computed_tokens, "hit_rate": r.hit_rate}
+    out["seconds"] = time.perf_counter() - t0
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -261,6 +292,7 @@ def main():
                       "calls_per_s": run.history_ops / max(run.history_seconds, 1e-9),
                       "plan_batch_ms": run.plan_seconds * 1e3},
     }
+    line["scheduler"] = scheduler_report(sc)
     if not args.no_cpu_baseline:
         log("[bench] timing the oracle on host cores")
         line["cpu_baseline"] = cpu_baseline(sc, inp, args.cpu_budget)

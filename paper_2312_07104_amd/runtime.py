@@ -11,6 +11,12 @@ through ``req_to_token``.  A request whose context is not fully cached gets
 slots for the missing part inserted first, standing in for the prefill that
 produced it earlier.
 
+``CacheAwareScheduler`` is Algorithm 1's admission loop (cache-aware,
+longest-shared-prefix-first scheduling with continuous batching, section 3 and
+Appendix A.2), and ``run_offline`` processes a fixed batch one request at a
+time in a chosen order, the setting of Theorem 3.1 (Appendix A.3), with
+hit-rate accounting.
+
 Every tree and pool operation runs in the native library; this module only
 sequences the calls and lays out the tables.
 """
@@ -113,3 +119,178 @@ def build_table(rows: list[np.ndarray], stride: int | None = None, row_order=Non
     for r, row in enumerate(rows):
         table[order[r], : len(row)] = row
     return table, order
+
+
+# ---- cache-aware scheduling (Algorithm 1, Theorem 3.1) ------------------------
+
+POLICIES = ("lspf", "fcfs", "random")
+
+
+@dataclass
+class Request:
+    """A request of the scheduler: prefill tokens plus a number of tokens it
+    will generate (their slots are reserved at admission)."""
+    rid: int
+    tokens: np.ndarray
+    out_len: int = 0
+    node: int = 0
+    prefix_len: int = 0
+    prefix_slots: np.ndarray | None = None
+    slots: np.ndarray | None = None
+
+    def size(self) -> int:
+        return int(self.tokens.shape[0]) + self.out_len
+
+
+def _order(policy: str, items: list, keys: list[int], rng) -> list:
+    """Longest matched prefix first (ties keep submission order), submission
+    order, or a seeded random order."""
+    if policy == "lspf":
+        idx = sorted(range(len(items)), key=lambda i: -keys[i])
+    elif policy == "fcfs":
+        idx = list(range(len(items)))
+    elif policy == "random":
+        idx = list(rng.permutation(len(items)))
+    else:
+        raise ValueError(f"unknown policy {policy!r}; one of {POLICIES}")
+    return [items[i] for i in idx]
+
+
+class CacheAwareScheduler:
+    """Algorithm 1: match every waiting request, sort by matched prefix length,
+    admit requests while ``size + current_size < available_size`` (locking each
+    admitted prefix lowers the available size by the tokens that stop being
+    evictable), allocate the new tokens' slots for the admitted requests
+    (evicting the needed size and retrying once when the pool is short), and on
+    completion unlock the prefix and insert the finished sequence.
+
+    ``current_size`` grows by each admitted request's size; the printed
+    pseudocode never updates it (reading 6 of the design notes).  Counters:
+    ``prefill_tokens`` (prompt tokens of admitted requests) and
+    ``cached_prefill_tokens`` (of those, found in the cache at admission);
+    ``hit_rate`` is their ratio.
+    """
+
+    def __init__(self, pool_slots: int, free_order=None, policy: str = "lspf", seed: int = 0):
+        if policy not in POLICIES:
+            raise ValueError(f"unknown policy {policy!r}; one of {POLICIES}")
+        self.cache = RadixCache(pool_slots, free_order)
+        self.policy = policy
+        self.rng = np.random.default_rng(seed)
+        self.waiting: list[Request] = []
+        self.running: list[Request] = []
+        self.prefill_tokens = 0
+        self.cached_prefill_tokens = 0
+        self._next_id = 0
+
+    @property
+    def hit_rate(self) -> float:
+        return self.cached_prefill_tokens / self.prefill_tokens if self.prefill_tokens else 0.0
+
+    def submit(self, tokens, out_len: int = 0) -> Request:
+        r = Request(self._next_id, np.ascontiguousarray(tokens, dtype=np.int32), int(out_len))
+        self._next_id += 1
+        self.waiting.append(r)
+        return r
+
+    def schedule(self) -> list[Request]:
+        """One pass of the admission loop; returns the requests admitted, each
+        with ``slots`` covering its prompt and reserved output positions."""
+        reqs = self.waiting
+        for r in reqs:
+            r.node, r.prefix_len, r.prefix_slots = self.cache.match_prefix(r.tokens)
+        ordered = _order(self.policy, reqs, [r.prefix_len for r in reqs], self.rng)
+        available = self.cache.evictable_size() + self.cache.available_size()
+        current = 0
+        batch = []
+        for r in ordered:
+            if r.size() + current < available:
+                batch.append(r)
+                available += self.cache.inc_ref(r.node)
+                current += r.size()
+        chosen = {r.rid for r in batch}
+        self.waiting = [r for r in reqs if r.rid not in chosen]
+        needed = sum(r.size() - r.prefix_len for r in batch)
+        if needed:
+            try:
+                buf = self.cache.alloc(needed)
+            except OutOfSlots:
+                self.cache.evict(needed)
+                buf = self.cache.alloc(needed)
+        else:
+            buf = np.empty(0, dtype=np.int32)
+        off = 0
+        for r in batch:
+            k = r.size() - r.prefix_len
+            r.slots = np.concatenate([r.prefix_slots, buf[off: off + k]]).astype(np.int32)
+            off += k
+            self.prefill_tokens += int(r.tokens.shape[0])
+            self.cached_prefill_tokens += r.prefix_len
+        self.running.extend(batch)
+        return batch
+
+    def finish(self, r: Request, generated=None) -> None:
+        """Unlock the request's prefix and insert prompt + generated tokens with
+        their slots; unused reserved slots go back to the pool."""
+        gen = np.zeros(0, dtype=np.int32) if generated is None else np.ascontiguousarray(generated, dtype=np.int32)
+        if gen.shape[0] > r.out_len:
+            raise ValueError("more generated tokens than reserved")
+        seq = np.concatenate([r.tokens, gen])
+        used = seq.shape[0]
+        self.cache.dec_ref(r.node)
+        self.cache.insert(seq, r.slots[:used])
+        if used < r.slots.shape[0]:
+            self.cache.free_slots(r.slots[used:])
+        self.running = [x for x in self.running if x.rid != r.rid]
+
+
+@dataclass
+class OfflineResult:
+    order: list[int]          # request indices in processing order
+    computed_tokens: int      # prefill tokens whose KV had to be computed
+    prefill_tokens: int
+
+    @property
+    def hit_rate(self) -> float:
+        return 1.0 - self.computed_tokens / self.prefill_tokens if self.prefill_tokens else 0.0
+
+
+def run_offline(sequences, pool_slots: int, policy: str = "lspf", seed: int = 0, free_order=None) -> OfflineResult:
+    """Processes a fixed batch one request at a time (Theorem 3.1's setting):
+    pick the next request by the policy (for ``lspf``, the one whose prompt
+    has the longest cached prefix right now), lock its cached prefix, compute
+    (allocate) the rest, insert, unlock.  Returns the order and the number of
+    computed tokens, which for ``lspf`` with ``pool_slots`` at least the longest
+    request equals the number of tokens on the edges of the batch's radix
+    tree."""
+    if policy not in POLICIES:
+        raise ValueError(f"unknown policy {policy!r}; one of {POLICIES}")
+    seqs = [np.ascontiguousarray(s, dtype=np.int32) for s in sequences]
+    cache = RadixCache(pool_slots, free_order)
+    rng = np.random.default_rng(seed)
+    remaining = list(range(len(seqs)))
+    if policy == "random":
+        remaining = [remaining[i] for i in rng.permutation(len(remaining))]
+    order, computed, total = [], 0, 0
+    while remaining:
+        if policy == "lspf":
+            lens = [cache.match_prefix(seqs[i])[1] for i in remaining]
+            k = max(range(len(remaining)), key=lambda j: (lens[j], -j))
+        else:
+            k = 0
+        i = remaining.pop(k)
+        node, m, slots = cache.match_prefix(seqs[i])
+        cache.inc_ref(node)
+        need = seqs[i].shape[0] - m
+        if need:
+            try:
+                new = cache.alloc(need)
+            except OutOfSlots:
+                cache.evict(need)
+                new = cache.alloc(need)
+            cache.insert(seqs[i], np.concatenate([slots, new]))
+        cache.dec_ref(node)
+        order.append(i)
+        computed += need
+        total += int(seqs[i].shape[0])
+    return OfflineResult(order, computed, total)
