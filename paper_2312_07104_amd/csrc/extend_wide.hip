@@ -28,6 +28,8 @@
 //     path has no cross-lane reduction.  Probabilities up to 2^24 cannot
 //     overflow the fp32 accumulators (2^24 times 2^22 keys times |v|).
 
+#include <type_traits>
+
 #include "device_common.h"
 #include "lds_dma.h"
 
@@ -46,6 +48,17 @@ constexpr float kLazyLog2 = 24.f;
 // for it: callers keep VALU writes of A and B at least two wait states away).
 __device__ __forceinline__ void pv_mfma(f32x4_t& o, const bf16x8_t& a, const bf16x8_t& b) {
   asm("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0" : "+a"(o) : "v"(a), "v"(b));
+}
+
+// S^T block (+)= K Q^T with the Q^T operand in AGPRs and S^T in VGPRs.  The
+// compiler inserts no wait states for it: VALU reads of S^T must come at
+// least 11 wait states after the last MFMA writing it (callers keep several
+// MFMAs in between, or an s_nop run).
+__device__ __forceinline__ void s_mfma_first(f32x4_t& s, const bf16x8_t& a, const bf16x8_t& qa) {
+  asm("v_mfma_f32_16x16x32_bf16 %0, %1, %2, 0" : "=&v"(s) : "v"(a), "a"(qa));
+}
+__device__ __forceinline__ void s_mfma_acc(f32x4_t& s, const bf16x8_t& a, const bf16x8_t& qa) {
+  asm("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0" : "+v"(s) : "v"(a), "a"(qa));
 }
 
 template <int D>
@@ -255,15 +268,9 @@ __global__ __launch_bounds__(512, 1) void extend_wide_kernel(
   for (int e = 0; e < 2; ++e) voff[e] = vr * 64 + 16 * ((2 * e + ((c & 3) >> 1)) ^ ra_kv_swz(vr)) + 8 * (c & 1);
 
   // S^T of one 32-key half: s[bb][j], element i = key 32 k2 + 8 g4 + 4 bb + i.
-  // The S^T MFMAs run at raised wave priority, so the SIMD's arbiter issues
-  // them ahead of the other wave's softmax VALU work.
+  // (Prologue only; the main loop computes S^T inside the fused step.)
   auto compute_s = [&](f32x4_t (&s)[2][kQB], int tile, int k2) {
-    __builtin_amdgcn_s_setprio(1);
     const unsigned char* kst = kv_lds + (tile % kStages) * STAGE_B;
-#pragma unroll
-    for (int bb = 0; bb < 2; ++bb)
-#pragma unroll
-      for (int j = 0; j < kQB; ++j) s[bb][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
@@ -271,31 +278,42 @@ __global__ __launch_bounds__(512, 1) void extend_wide_kernel(
         const bf16x8_t a = __builtin_bit_cast(
             bf16x8_t, *reinterpret_cast<const uint4*>(kst + koff + ks * GROUP_B + (32 * k2 + 4 * bb) * 64));
 #pragma unroll
-        for (int j = 0; j < kQB; ++j) s[bb][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qT[j][ks], s[bb][j], 0, 0, 0);
+        for (int j = 0; j < kQB; ++j) {
+          if (ks == 0) s_mfma_first(s[bb][j], a, qT[j][ks]);
+          else s_mfma_acc(s[bb][j], a, qT[j][ks]);
+        }
       }
-    __builtin_amdgcn_s_setprio(0);
+    // let the last MFMAs retire before the VALU reads S^T
+    asm volatile("s_nop 7\n\ts_nop 7" : "+v"(s[0][0]), "+v"(s[1][kQB - 1]));
   };
 
-  // Softmax of one half into P^T (bf16), then O^T += V^T P^T.
-  auto softmax_pv = [&](f32x4_t (&s)[2][kQB], int tile, int k2) {
+  // Maximum of one half's scores per query column (this lane's 8 keys).
+  auto half_max = [&](f32x4_t (&s)[2][kQB], int j) {
+    float m = __builtin_fmaxf(__builtin_fmaxf(s[0][j][0], s[0][j][1]), s[0][j][2]);
+    m = __builtin_fmaxf(__builtin_fmaxf(m, s[0][j][3]), s[1][j][0]);
+    m = __builtin_fmaxf(__builtin_fmaxf(m, s[1][j][1]), s[1][j][2]);
+    return __builtin_fmaxf(m, s[1][j][3]);
+  };
+
+  // After a half's S^T is complete and its per-lane maxima mt are known:
+  // causal mask (diagonal halves only, maxima recomputed), then the rare move
+  // of the running maximum with its rescale of O^T.
+  auto pre = [&](f32x4_t (&s)[2][kQB], int tile, int k2, float (&mt)[kQB]) {
     const int kh = tile * kBN + 32 * k2;  // first key of the half
     if (kh + 31 > P + tok0) {
 #pragma unroll
-      for (int j = 0; j < kQB; ++j)
+      for (int j = 0; j < kQB; ++j) {
 #pragma unroll
         for (int bb = 0; bb < 2; ++bb)
 #pragma unroll
           for (int i = 0; i < 4; ++i)
             if (kh + 8 * g4 + 4 * bb + i > qlim[j]) s[bb][j][i] = -INFINITY;
+        mt[j] = half_max(s, j);
+      }
     }
-    float mt[kQB];
     bool up = false;
 #pragma unroll
-    for (int j = 0; j < kQB; ++j) {
-      mt[j] = fmaxf(fmaxf(fmaxf(s[0][j][0], s[0][j][1]), fmaxf(s[0][j][2], s[0][j][3])),
-                    fmaxf(fmaxf(s[1][j][0], s[1][j][1]), fmaxf(s[1][j][2], s[1][j][3])));
-      up |= mt[j] > thr[j];
-    }
+    for (int j = 0; j < kQB; ++j) up |= mt[j] > thr[j];
     if (__builtin_amdgcn_ballot_w64(up) != 0) {
       // Rare: some column's maximum passed its threshold.  Move those
       // columns' maxima and rescale their O^T.  The nops give the last
@@ -330,61 +348,131 @@ __global__ __launch_bounds__(512, 1) void extend_wide_kernel(
         }
       }
     }
-    bf16x8_t pT[kQB];
-#pragma unroll
-    for (int j = 0; j < kQB; ++j) {
-      float p[8];
+  };
+
+  // One software-pipelined step over two halves, written in issue order:
+  // the S^T MFMAs of the next half sn, each followed by one probability of
+  // the current half sc (fma + exp, pack every second), with the K operand
+  // reads two k-steps ahead and the V^T reads of the current half in the
+  // second part; then the current half's PV MFMAs (AGPR accumulators, inline
+  // assembly), the next half's per-lane maxima slotted between them.
+  // sched_barrier(0) fences keep the scheduler from regrouping the MFMAs and
+  // the VALU work, so the matrix core stays busy while the exponentials issue.
+  // HAS_NEXT = false is the last half of the item (no S^T to compute).
+  auto fused = [&](auto has_next, f32x4_t (&sn)[2][kQB], int tile_n, int k2_n, f32x4_t (&sc)[2][kQB], int tile_c,
+                   int k2_c, float (&mt)[kQB]) {
+    constexpr bool HAS_NEXT = decltype(has_next)::value;
+    constexpr int NS = 2 * KS * kQB;  // S^T MFMAs of one half
+    constexpr int NP = 8 * kQB;       // probabilities per lane per half
+    constexpr int VA = 3;             // V^T operands (16-row blocks) read ahead of their PV step
+    const unsigned char* kst = kv_lds + (tile_n % kStages) * STAGE_B + koff + 32 * k2_n * 64;
+    const unsigned char* vst = kv_lds + (tile_c % kStages) * STAGE_B + TILE_B + 32 * k2_c * 64;
+    bf16x8_t kf[KS][2];
+    bf16x4_t vf[DB][2];
+    float p[NP];
+    uint32_t pw[NP / 2];
+    auto read_k = [&](int ks) {
 #pragma unroll
       for (int bb = 0; bb < 2; ++bb)
+        kf[ks][bb] = __builtin_bit_cast(bf16x8_t,
+                                        *reinterpret_cast<const uint4*>(kst + ks * GROUP_B + 4 * bb * 64));
+    };
+    auto read_v = [&](int db) {
+      const unsigned char* vb = vst + voff[db & 1] + (db >> 1) * GROUP_B;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) p[4 * bb + i] = ra_exp2(__builtin_fmaf(s[bb][j][i], scale_log2, mb[j]));
-      uint4 w;
-      w.x = ra_pack_bf16x2(p[0], p[1]);
-      w.y = ra_pack_bf16x2(p[2], p[3]);
-      w.z = ra_pack_bf16x2(p[4], p[5]);
-      w.w = ra_pack_bf16x2(p[6], p[7]);
-      pT[j] = __builtin_bit_cast(bf16x8_t, w);
+      for (int h = 0; h < 2; ++h)
+        vf[db][h] =
+            __builtin_amdgcn_ds_read_tr16_b64_v4bf16((__attribute__((address_space(3))) bf16x4_t*)(vb + h * 4 * 64));
+    };
+    auto prob = [&](int v) {  // v = 8 j + 4 bb + i
+      const int j = v >> 3, bb = (v >> 2) & 1, i = v & 3;
+      p[v] = ra_exp2(__builtin_fmaf(sc[bb][j][i], scale_log2, mb[j]));
+      if (v & 1) pw[v >> 1] = ra_pack_bf16x2(p[v - 1], p[v]);
+    };
+    if constexpr (HAS_NEXT) {
+      read_k(0);
+      if constexpr (KS > 1) read_k(1);
+      __builtin_amdgcn_sched_barrier(0);
+      constexpr int PPG = (NP + NS - 1) / NS;  // probabilities per S^T MFMA
+#pragma unroll
+      for (int n = 0; n < NS; ++n) {
+        const int ks = n / (2 * kQB), bb = (n / kQB) & 1, j = n % kQB;
+        if (ks == 0) s_mfma_first(sn[bb][j], kf[ks][bb], qT[j][ks]);
+        else s_mfma_acc(sn[bb][j], kf[ks][bb], qT[j][ks]);
+#pragma unroll
+        for (int v = n * PPG; v < (n + 1) * PPG && v < NP; ++v) prob(v);
+        if (n % (2 * kQB) == 2 * kQB - 1 && ks + 2 < KS) read_k(ks + 2);
+        // the first V^T operands, spread over the last S^T MFMAs
+        if (n >= NS - VA && n - (NS - VA) < DB) read_v(n - (NS - VA));
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    } else {
+#pragma unroll
+      for (int db = 0; db < VA && db < DB; ++db) read_v(db);
+#pragma unroll
+      for (int v = 0; v < NP; ++v) prob(v);
     }
+    bf16x8_t pT[kQB];
+#pragma unroll
+    for (int j = 0; j < kQB; ++j)
+      pT[j] = __builtin_bit_cast(bf16x8_t, make_uint4(pw[4 * j], pw[4 * j + 1], pw[4 * j + 2], pw[4 * j + 3]));
     // two wait states between the VALU writes of P^T and the MFMAs reading it
     asm volatile("s_nop 1" : "+v"(pT[0]), "+v"(pT[1]), "+v"(ones));
-    const unsigned char* vst = kv_lds + (tile % kStages) * STAGE_B + TILE_B + 32 * k2 * 64;
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int db = 0; db < DB; ++db) {
-      const unsigned char* vb = vst + voff[db & 1] + (db >> 1) * GROUP_B;
-      const bf16x4_t lo =
-          __builtin_amdgcn_ds_read_tr16_b64_v4bf16((__attribute__((address_space(3))) bf16x4_t*)(vb));
-      const bf16x4_t hi =
-          __builtin_amdgcn_ds_read_tr16_b64_v4bf16((__attribute__((address_space(3))) bf16x4_t*)(vb + 4 * 64));
-      const bf16x8_t a = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+      if (db + VA < DB) read_v(db + VA);
+      const bf16x8_t a = __builtin_shufflevector(vf[db][0], vf[db][1], 0, 1, 2, 3, 4, 5, 6, 7);
 #pragma unroll
       for (int j = 0; j < kQB; ++j) pv_mfma(o[db][j], a, pT[j]);
+      // the next half's maxima, one column per PV step once its S^T has retired
+      if constexpr (HAS_NEXT) {
+        if (db >= 2 && db - 2 < kQB) mt[db - 2] = half_max(sn, db - 2);
+      }
+      __builtin_amdgcn_sched_barrier(0);
     }
 #pragma unroll
     for (int j = 0; j < kQB; ++j) pv_mfma(o[DB][j], ones, pT[j]);
+    if constexpr (HAS_NEXT) {
+      if constexpr (DB - 2 < kQB) {
+#pragma unroll
+        for (int j = (DB - 2 > 0 ? DB - 2 : 0); j < kQB; ++j) mt[j] = half_max(sn, j);
+      }
+    }
   };
 
-  // ---- main loop: half h's softmax and PV run beside half h+1's S^T --------
+  // ---- main loop: half h's exponentials and PV run beside half h+1's S^T ---
   // Ping-pong: waves 4..7 take each tile's barrier at the start of their
   // iteration, waves 0..3 in its middle (the latest point before the S^T of
   // the next tile).  The barrier aligns the two points, so the second group
   // runs half an iteration behind the first and the two waves sharing a SIMD
-  // are in different phases (one in its softmax while the other issues MFMAs).
-  // Either point is after the wave's last read of the stage being refilled.
+  // are in different phases.  Either point is after the wave's last read of
+  // the stage being refilled.
   const bool lead = wave < kWaves / 2;
+  using yes = std::integral_constant<bool, true>;
+  using no = std::integral_constant<bool, false>;
   f32x4_t sa[2][kQB], sb[2][kQB];
+  float mt[kQB];
   tile_top(0);
   compute_s(sa, 0, 0);
-  for (int t = 0; t < n_tiles; ++t) {
-    const bool more = t + 1 < n_tiles;
-    if (!lead && more) tile_top(t + 1);
-    compute_s(sb, t, 1);
-    softmax_pv(sa, t, 0);
-    if (more) {
-      if (lead) tile_top(t + 1);
-      compute_s(sa, t + 1, 0);
-    }
-    softmax_pv(sb, t, 1);
+#pragma unroll
+  for (int j = 0; j < kQB; ++j) mt[j] = half_max(sa, j);
+  pre(sa, 0, 0, mt);
+  // The last tile is peeled off the loop so that no branch inside it has two
+  // sides computing the same probabilities (the compiler would hoist them out
+  // of the fused step).
+  int t = 0;
+  for (; t + 1 < n_tiles; ++t) {
+    if (!lead) tile_top(t + 1);
+    fused(yes{}, sb, t, 1, sa, t, 0, mt);
+    pre(sb, t, 1, mt);
+    if (lead) tile_top(t + 1);
+    fused(yes{}, sa, t + 1, 0, sb, t, 1, mt);
+    pre(sa, t + 1, 0, mt);
   }
+  fused(yes{}, sb, t, 1, sa, t, 0, mt);
+  pre(sb, t, 1, mt);
+  fused(no{}, sa, 0, 0, sb, t, 1, mt);
 
   // No copy may still be landing in LDS once the work-group ends (the last
   // index copies were issued past the final tile).
