@@ -109,7 +109,7 @@ __global__ __launch_bounds__(512, 1) void extend_wide_kernel(
   const int n_tiles = (kend + kBN - 1) / kBN;
 
   const int tid = threadIdx.x;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform (SGPR)
   const int lane = tid & 63;
   const int c = lane & 15;
   const int g4 = lane >> 4;
@@ -154,29 +154,48 @@ __global__ __launch_bounds__(512, 1) void extend_wide_kernel(
     const int pos = tile * kBN + idx_pos;
     ra_dma4(trow + (tile < n_tiles && pos < P ? pos : 0), ra_lds_addr(&idx_lds[tile % kRing][0]));
   };
-  // K and V rows of one tile into stage tile % kStages: 2 * LOADS copies per
-  // wave for every tile < n_tiles.
-  auto issue_kv = [&](int tile) {
-    if (tile >= n_tiles) return;
+  // This lane's LOADS slot indices of a tile, read from the index ring (one
+  // vector LDS read; the values are consumed a tile later).
+  auto read_idx = [&](int tile, int32_t (&sl)[LOADS]) {
+    const int32_t* w = &idx_lds[tile % kRing][LOADS * u0];
+    if constexpr (LOADS == 2) {
+      const int2 v = *reinterpret_cast<const int2*>(w);
+      sl[0] = v.x, sl[1] = v.y;
+    } else {
+      sl[0] = w[0];
+    }
+  };
+  // Copies of one tile's K and V rows into stage tile % kStages: 2 * LOADS
+  // per wave (source address per lane, LDS base per wave), K then V for each
+  // it.  sl = the tile's slot indices (read_idx).  A tile past the last one
+  // gets dummy copies of slot 0's row (one cache line per copy) into its
+  // stage, which no wave reads again, so every tile has the same number of
+  // outstanding loads.
+  struct KvCopies {
+    uint64_t src[2 * LOADS];
+    uint32_t lds[2 * LOADS];
+  };
+  auto prep_kv = [&](int tile, const int32_t (&sl)[LOADS], KvCopies& cp) {
     const int kb = tile * kBN;
     const uint32_t kst = lds_kv0 + (tile % kStages) * STAGE_B;
-    int32_t sl[LOADS];
-    if (kb < P) {
-      const int32_t* w = &idx_lds[tile % kRing][LOADS * u0];
-      if constexpr (LOADS == 2) {
-        const int2 v = *reinterpret_cast<const int2*>(w);
-        sl[0] = v.x, sl[1] = v.y;
-      } else {
-        sl[0] = w[0];
-      }
+#pragma unroll
+    for (int it = 0; it < LOADS; ++it) {
+      cp.lds[2 * it] = kst + dma_lds[it];
+      cp.lds[2 * it + 1] = kst + TILE_B + dma_lds[it];
     }
-    if (kb + kBN <= P) {
+    if (tile >= n_tiles) {
+#pragma unroll
+      for (int it = 0; it < LOADS; ++it) {
+        cp.src[2 * it] = kpool_lane[it];
+        cp.src[2 * it + 1] = kpool_lane[it] + vpool_delta;
+      }
+    } else if (kb + kBN <= P) {
 #pragma unroll
       for (int it = 0; it < LOADS; ++it) {
         const uint32_t slot = min(static_cast<uint32_t>(sl[it]), smax);  // negative -> clamped
         const uint64_t src = kpool_lane[it] + static_cast<uint64_t>(slot) * row_bytes;
-        ra_dma16(reinterpret_cast<const void*>(src), kst + dma_lds[it]);
-        ra_dma16(reinterpret_cast<const void*>(src + vpool_delta), kst + TILE_B + dma_lds[it]);
+        cp.src[2 * it] = src;
+        cp.src[2 * it + 1] = src + vpool_delta;
       }
     } else {
 #pragma unroll
@@ -192,27 +211,37 @@ __global__ __launch_bounds__(512, 1) void extend_wide_kernel(
           src = knew_lane[it] + static_cast<uint64_t>(pos) * row_bytes;
           vdelta = vnew_delta;
         }
-        ra_dma16(reinterpret_cast<const void*>(src), kst + dma_lds[it]);
-        ra_dma16(reinterpret_cast<const void*>(src + vdelta), kst + TILE_B + dma_lds[it]);
+        cp.src[2 * it] = src;
+        cp.src[2 * it + 1] = src + vdelta;
       }
     }
   };
-  // Top of tile u: K/V(u) and the indices needed next are in LDS for every
-  // wave, stage (u - 2) % kStages is free; refill it and extend the index
-  // ring.  Outstanding loads of this wave, oldest first: the group issued at
-  // the top of u - 2 (K/V(u), idx(u + 2)) and the group of u - 1
-  // (K/V(u + 1) if it exists, idx(u + 3)); the wait retires all but the
-  // latter.  Tile 0 follows the prologue, whose groups hold no index copy.
+  auto issue_copy = [&](const KvCopies& cp, int i) {
+    ra_dma16(reinterpret_cast<const void*>(cp.src[i]), cp.lds[i]);
+  };
+  // Top of tile u: K/V(u) is in LDS for every wave and stage (u + 2) %
+  // kStages = (u - 2) % kStages is free.  Order of this wave's loads issued
+  // since the top of u - 1: idx(u + 3) (wave 0 only), then the copies of
+  // K/V(u + 1); the wait retires everything before those, so idx(u + 3) and
+  // K/V(u) have landed, and the barrier makes them visible to all waves.
+  // Then: the index copy of tile u + 4 (into the ring slot of tile u, whose
+  // indices were read at the top of u - 3), the read of tile u + 3's indices
+  // into registers (used at the top of u + 1, so no wait on it here), and the
+  // addresses of tile u + 2's copies from the indices read at the top of
+  // u - 1.  The copies themselves are issued by the next fused step, spread
+  // over its PV MFMAs, so the eight waves do not queue their copies at the
+  // address unit all at once after the barrier.
+  int32_t sl_next[LOADS];  // slot indices of the tile whose copies are prepared next
+  KvCopies cp;
   auto tile_top = [&](int u) {
-    const bool next = u + 1 < n_tiles;
-    if (u == 0 || wave != 0) {
-      if (next) ra_wait_vmcnt<2 * LOADS>(); else ra_wait_vmcnt<0>();
-    } else {
-      if (next) ra_wait_vmcnt<2 * LOADS + 1>(); else ra_wait_vmcnt<1>();
-    }
-    __syncthreads();
-    issue_kv(u + 2);
+    ra_wait_vmcnt<2 * LOADS>();
+    __builtin_amdgcn_s_barrier();
     issue_idx(u + 4);
+    int32_t sl[LOADS];
+#pragma unroll
+    for (int it = 0; it < LOADS; ++it) sl[it] = sl_next[it];
+    read_idx(u + 3, sl_next);
+    prep_kv(u + 2, sl, cp);
   };
 
   // Q^T operands of the wave's four 16-query column blocks.
@@ -237,8 +266,18 @@ __global__ __launch_bounds__(512, 1) void extend_wide_kernel(
   for (int t = 0; t < kRing; ++t) issue_idx(t);
   ra_wait_vmcnt<0>();
   __syncthreads();
-  issue_kv(0);
-  issue_kv(1);
+  {
+    int32_t sl0[LOADS], sl1[LOADS];
+    read_idx(0, sl0);
+    read_idx(1, sl1);
+    read_idx(2, sl_next);
+    prep_kv(0, sl0, cp);
+#pragma unroll
+    for (int i = 0; i < 2 * LOADS; ++i) issue_copy(cp, i);
+    prep_kv(1, sl1, cp);
+#pragma unroll
+    for (int i = 0; i < 2 * LOADS; ++i) issue_copy(cp, i);
+  }
 
   f32x4_t o[DB + 1][kQB];  // O^T blocks; block DB holds the row sums (A operand = ones)
 #pragma unroll
@@ -359,9 +398,18 @@ __global__ __launch_bounds__(512, 1) void extend_wide_kernel(
   // sched_barrier(0) fences keep the scheduler from regrouping the MFMAs and
   // the VALU work, so the matrix core stays busy while the exponentials issue.
   // HAS_NEXT = false is the last half of the item (no S^T to compute).
-  auto fused = [&](auto has_next, f32x4_t (&sn)[2][kQB], int tile_n, int k2_n, f32x4_t (&sc)[2][kQB], int tile_c,
-                   int k2_c, float (&mt)[kQB]) {
+  // kpre holds the K operands of sn's first two k-steps (read by the previous
+  // step); at the end of the PV part the step reads those of the half after
+  // sn, (tile_f, k2_f), when pf is set (its tile is resident by then).
+  constexpr int KP = KS > 1 ? 2 : 1;  // k-steps prefetched across steps
+  // with_copies: issue the copies prepared by the last tile_top, one every
+  // DB / (2 LOADS) PV steps.
+  auto fused = [&](auto has_next, auto with_copies, f32x4_t (&sn)[2][kQB], int tile_n, int k2_n,
+                   f32x4_t (&sc)[2][kQB], int tile_c, int k2_c, float (&mt)[kQB], bf16x8_t (&kpre)[KP][2], bool pf,
+                   int tile_f, int k2_f) {
     constexpr bool HAS_NEXT = decltype(has_next)::value;
+    constexpr bool COPIES = decltype(with_copies)::value;
+    constexpr int CSTEP = DB / (2 * LOADS) > 0 ? DB / (2 * LOADS) : 1;
     constexpr int NS = 2 * KS * kQB;  // S^T MFMAs of one half
     constexpr int NP = 8 * kQB;       // probabilities per lane per half
     constexpr int VA = 3;             // V^T operands (16-row blocks) read ahead of their PV step
@@ -390,8 +438,10 @@ __global__ __launch_bounds__(512, 1) void extend_wide_kernel(
       if (v & 1) pw[v >> 1] = ra_pack_bf16x2(p[v - 1], p[v]);
     };
     if constexpr (HAS_NEXT) {
-      read_k(0);
-      if constexpr (KS > 1) read_k(1);
+#pragma unroll
+      for (int ks = 0; ks < KP; ++ks)
+#pragma unroll
+        for (int bb = 0; bb < 2; ++bb) kf[ks][bb] = kpre[ks][bb];
       __builtin_amdgcn_sched_barrier(0);
       constexpr int PPG = (NP + NS - 1) / NS;  // probabilities per S^T MFMA
 #pragma unroll
@@ -429,10 +479,26 @@ __global__ __launch_bounds__(512, 1) void extend_wide_kernel(
       if constexpr (HAS_NEXT) {
         if (db >= 2 && db - 2 < kQB) mt[db - 2] = half_max(sn, db - 2);
       }
+      if constexpr (COPIES) {
+        if (db % CSTEP == CSTEP - 1 && db / CSTEP < 2 * LOADS) issue_copy(cp, db / CSTEP);
+      }
       __builtin_amdgcn_sched_barrier(0);
     }
 #pragma unroll
     for (int j = 0; j < kQB; ++j) pv_mfma(o[DB][j], ones, pT[j]);
+    if constexpr (COPIES) {
+#pragma unroll
+      for (int i = DB / CSTEP; i < 2 * LOADS; ++i) issue_copy(cp, i);
+    }
+    if (pf) {
+      const unsigned char* kf_st = kv_lds + (tile_f % kStages) * STAGE_B + koff + 32 * k2_f * 64;
+#pragma unroll
+      for (int ks = 0; ks < KP; ++ks)
+#pragma unroll
+        for (int bb = 0; bb < 2; ++bb)
+          kpre[ks][bb] = __builtin_bit_cast(bf16x8_t,
+                                            *reinterpret_cast<const uint4*>(kf_st + ks * GROUP_B + 4 * bb * 64));
+    }
     if constexpr (HAS_NEXT) {
       if constexpr (DB - 2 < kQB) {
 #pragma unroll
@@ -442,37 +508,44 @@ __global__ __launch_bounds__(512, 1) void extend_wide_kernel(
   };
 
   // ---- main loop: half h's exponentials and PV run beside half h+1's S^T ---
-  // Ping-pong: waves 4..7 take each tile's barrier at the start of their
-  // iteration, waves 0..3 in its middle (the latest point before the S^T of
-  // the next tile).  The barrier aligns the two points, so the second group
-  // runs half an iteration behind the first and the two waves sharing a SIMD
-  // are in different phases.  Either point is after the wave's last read of
-  // the stage being refilled.
-  const bool lead = wave < kWaves / 2;
+  // Every wave takes the tile barrier at the top of its iteration.  The K
+  // operands of each step's first two k-steps were read at the end of the
+  // step before (for the first half of tile t + 1 that read comes after the
+  // barrier of the top of t + 1, so the tile is resident).
   using yes = std::integral_constant<bool, true>;
   using no = std::integral_constant<bool, false>;
   f32x4_t sa[2][kQB], sb[2][kQB];
   float mt[kQB];
+  bf16x8_t kpre[KP][2];
   tile_top(0);
+#pragma unroll
+  for (int i = 0; i < 2 * LOADS; ++i) issue_copy(cp, i);
   compute_s(sa, 0, 0);
 #pragma unroll
   for (int j = 0; j < kQB; ++j) mt[j] = half_max(sa, j);
+  {
+    const unsigned char* k1 = kv_lds + koff + 32 * 64;  // tile 0, half 1
+#pragma unroll
+    for (int ks = 0; ks < KP; ++ks)
+#pragma unroll
+      for (int bb = 0; bb < 2; ++bb)
+        kpre[ks][bb] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const uint4*>(k1 + ks * GROUP_B + 4 * bb * 64));
+  }
   pre(sa, 0, 0, mt);
   // The last tile is peeled off the loop so that no branch inside it has two
   // sides computing the same probabilities (the compiler would hoist them out
   // of the fused step).
   int t = 0;
   for (; t + 1 < n_tiles; ++t) {
-    if (!lead) tile_top(t + 1);
-    fused(yes{}, sb, t, 1, sa, t, 0, mt);
+    tile_top(t + 1);
+    fused(yes{}, yes{}, sb, t, 1, sa, t, 0, mt, kpre, true, t + 1, 0);
     pre(sb, t, 1, mt);
-    if (lead) tile_top(t + 1);
-    fused(yes{}, sa, t + 1, 0, sb, t, 1, mt);
+    fused(yes{}, no{}, sa, t + 1, 0, sb, t, 1, mt, kpre, true, t + 1, 1);
     pre(sa, t + 1, 0, mt);
   }
-  fused(yes{}, sb, t, 1, sa, t, 0, mt);
+  fused(yes{}, no{}, sb, t, 1, sa, t, 0, mt, kpre, false, 0, 0);
   pre(sb, t, 1, mt);
-  fused(no{}, sa, 0, 0, sb, t, 1, mt);
+  fused(no{}, no{}, sa, 0, 0, sb, t, 1, mt, kpre, false, 0, 0);
 
   // No copy may still be landing in LDS once the work-group ends (the last
   // index copies were issued past the final tile).
