@@ -84,11 +84,18 @@ def algorithmic_work(sc, inp):
     pairs = sum(e * p + e * (e + 1) // 2 for _, p, e, _ in inp.ext_meta)
     ext_flops = 4.0 * d * hq * pairs
     ext_bytes = sum((p + e) * (2 * hkv * d * 2) + p * 4 + e * (2 * hq * d * 2) for _, p, e, _ in inp.ext_meta)
+    # distinct K/V rows over the extend contexts (a position is named by the
+    # hash of its prefix, so requests sharing a prefix share its rows)
+    from workload import contentgen as cg
+    seen = set()
+    for h in cg.prefix_hashes_batch([toks[:p + e] for toks, p, e, _ in inp.ext_meta], sc.seed) if inp.ext_meta else []:
+        seen.update(h.tolist())
+    ext_unique_bytes = len(seen) * (2 * hkv * d * 2) + sum(e * (2 * hq * d * 2) for _, _, e, _ in inp.ext_meta)
     sum_l = sum(l for _, l in inp.dec_meta)
     dec_bytes = sum_l * (2 * hkv * d * 2 + 4) + inp.n_dec * 2 * hq * d * 2
     dec_flops = 4.0 * d * hq * sum_l
     attended = sum(p + e for _, p, e, _ in inp.ext_meta) + sum_l
-    return dict(ext_flops=ext_flops, ext_bytes=ext_bytes, dec_bytes=dec_bytes, dec_flops=dec_flops,
+    return dict(ext_flops=ext_flops, ext_bytes=ext_bytes, ext_unique_bytes=ext_unique_bytes, dec_bytes=dec_bytes, dec_flops=dec_flops,
                 attended=attended, sum_l=sum_l, pairs=pairs)
 
 
@@ -161,6 +168,9 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="mixed")
+    ap.add_argument("--phase", type=int, default=0,
+                    help="batch of the workload to time; earlier batches run and finish first (their new tokens "
+                         "are stored and their sequences inserted)")
     ap.add_argument("--cpu-budget", type=float, default=20.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
@@ -181,7 +191,11 @@ def main():
     log(f"[bench] workload={sc.name} seed={sc.seed} Hq={sc.hq} Hkv={sc.hkv} D={sc.d} S={sc.pool_slots}")
     run = ScenarioRun(sc)
     log(f"[bench] history: {sc.history_len} requests, {run.history_ops} tree calls, {run.history_seconds:.2f} s")
-    inp = run.prepare(0)
+    for ph in range(args.phase):
+        prev = run.prepare(ph)
+        run.store(prev)
+        run.finish(ph, prev)
+    inp = run.prepare(args.phase)
     log(f"[bench] batch planned: {run.plan_seconds * 1e3:.1f} ms host, hit rate {inp.plan.hit_rate:.3f}")
     run.store(inp)  # the first pass writes new tokens' K/V (identical values every step)
     torch.cuda.synchronize()
@@ -240,29 +254,37 @@ def main():
     kernels = {
         "store_kv": {"ms": t_store, "tokens": int(n_new)},
         "extend": {"ms": t_ext, "tflops": work["ext_flops"] / (t_ext * 1e-3) / 1e12,
-                   "flops": work["ext_flops"]} if inp.n_ext else None,
+                   "flops": work["ext_flops"], "gbs": work["ext_bytes"] / (t_ext * 1e-3) / 1e9,
+                   "bytes": work["ext_bytes"], "unique_bytes": work["ext_unique_bytes"]} if inp.n_ext else None,
         "decode": {"ms": t_dec, "gbs": work["dec_bytes"] / (t_dec * 1e-3) / 1e9,
                    "bytes": work["dec_bytes"]} if inp.n_dec else None,
     }
-    if inp.n_ext and t_ext >= t_dec:
-        ach = work["ext_flops"] / (t_ext * 1e-3) / 1e12
-        roof = {"kernel": "extend", "bound": "mfma", "achieved": ach, "peak": BF16_PEAK_TFLOPS,
-                "unit": "TFLOP/s", "frac": ach / BF16_PEAK_TFLOPS, "traffic": measured_traffic("extend", sc.name)}
-    else:
-        ach = work["dec_bytes"] / (t_dec * 1e-3) / 1e9
-        roof = {"kernel": "decode", "bound": "hbm", "achieved": ach, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": ach / HBM_PEAK_GBS, "traffic": measured_traffic("decode", sc.name)}
-    # second roofline line for the other kernel (if the batch has it), same definitions
-    other = None
-    if roof["kernel"] == "extend" and kernels["decode"]:
-        other = {"kernel": "decode", "bound": "hbm", "achieved": kernels["decode"]["gbs"], "peak": HBM_PEAK_GBS,
-                 "unit": "GB/s"}
-    elif roof["kernel"] == "decode" and kernels["extend"]:
-        other = {"kernel": "extend", "bound": "mfma", "achieved": kernels["extend"]["tflops"],
-                 "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s"}
-    if other:
-        other["frac"] = other["achieved"] / other["peak"]
-        other["traffic"] = measured_traffic(other["kernel"], sc.name)
+
+    def extend_roof():
+        """Extend is bounded by MFMA when its algorithmic intensity (flops per
+        byte of distinct K/V rows, queries and outputs: a prefix shared by
+        several requests is fetched once and served from L2 / the Infinity
+        Cache) is above the ridge point of the two peaks, by HBM below it
+        (short extends over long cached prefixes).  The HBM figure itself is
+        the per-request byte count, like decode's."""
+        e = kernels["extend"]
+        if work["ext_flops"] / max(work["ext_unique_bytes"], 1) >= BF16_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9):
+            return {"kernel": "extend", "bound": "mfma", "achieved": e["tflops"], "peak": BF16_PEAK_TFLOPS,
+                    "unit": "TFLOP/s"}
+        return {"kernel": "extend", "bound": "hbm", "achieved": e["gbs"], "peak": HBM_PEAK_GBS, "unit": "GB/s"}
+
+    def decode_roof():
+        return {"kernel": "decode", "bound": "hbm", "achieved": kernels["decode"]["gbs"], "peak": HBM_PEAK_GBS,
+                "unit": "GB/s"}
+
+    # roofline: the kernel that takes longer; roofline_other: the other one
+    first, second = (extend_roof, decode_roof) if inp.n_ext and t_ext >= t_dec else (decode_roof, extend_roof)
+    roof = first()
+    other = second() if (kernels["decode"] if second is decode_roof else kernels["extend"]) else None
+    for r in (roof, other):
+        if r:
+            r["frac"] = r["achieved"] / r["peak"]
+            r["traffic"] = measured_traffic(r["kernel"], sc.name)
 
     if args.copy_calibration_mib:
         n = args.copy_calibration_mib << 20
@@ -279,7 +301,7 @@ def main():
         "value": value, "unit": "attended KV tokens/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": ms_step, "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
-        "config": {"workload": sc.name, "hq": sc.hq, "hkv": sc.hkv, "head_dim": sc.d,
+        "config": {"workload": sc.name, "phase": args.phase, "hq": sc.hq, "hkv": sc.hkv, "head_dim": sc.d,
                    "pool_slots": sc.pool_slots, "extend_requests": inp.n_ext, "decode_requests": inp.n_dec,
                    "sum_extend_tokens": inp.total_ext, "sum_decode_context": work["sum_l"],
                    "history_requests": sc.history_len, "tree_calls": run.history_ops,

@@ -196,3 +196,59 @@ def test_mixed_small_full():
     inp, oe, od = run_phase(run, 0)
     check_extend(run, inp, oe, what="mixed_small/extend")
     check_decode(run, inp, od, what="mixed_small/decode")
+
+
+# ------------------------------------------- jump-forward (small-E) extends -----
+
+def test_jump_forward_small_full():
+    sc = S.jump_forward_small()
+    log(f"case: jump_forward_small seed={sc.seed}")
+    run = ScenarioRun(sc)
+    inp, oe, _ = run_phase(run, 0)
+    assert max(e for _, _, e, _ in inp.ext_meta) <= 33
+    er = check_extend(run, inp, oe, what="jump_forward_small")
+    log("jump_forward_small worst", er)
+
+
+def test_jump_forward_sampled():
+    sc = S.jump_forward()
+    log(f"case: jump_forward seed={sc.seed}")
+    run = ScenarioRun(sc)
+    inp, oe, _ = run_phase(run, 0)
+    lens = np.array([e for _, _, e, _ in inp.ext_meta])
+    sample = sorted({int(lens.argmin()), int(lens.argmax()), 0, 101, 255})
+    er = check_extend(run, inp, oe, sample=sample, what="jump_forward")
+    log("jump_forward worst", er)
+
+
+# ----------------------------------------------- tensor-parallel head shards -----
+
+def test_tp8_mixed_shard_sampled():
+    sc = S.ALL["mixed_tp8"]()
+    log(f"case: mixed_tp8 seed={sc.seed} Hq={sc.hq} Hkv={sc.hkv}")
+    run = ScenarioRun(sc)
+    inp, oe, od = run_phase(run, 0)
+    check_extend(run, inp, oe, sample=[1, 30], rows_per_req=12, what="mixed_tp8/extend")
+    lens = np.array([l for _, l in inp.dec_meta])
+    check_decode(run, inp, od, sample=sorted({int(lens.argmax()), int(lens.argmin()), 77}), what="mixed_tp8/decode")
+
+
+def test_tp4_chat_shard_sampled():
+    sc = S.ALL["decode_chat_tp4"]()
+    log(f"case: decode_chat_tp4 seed={sc.seed} Hq={sc.hq} Hkv={sc.hkv}")
+    run = ScenarioRun(sc)
+    inp, _, od = run_phase(run, 0)
+    lens = np.array([l for _, l in inp.dec_meta])
+    check_decode(run, inp, od, sample=sorted({int(lens.argmax()), int(lens.argmin()), 9, 200}),
+                 what="decode_chat_tp4")
+
+
+def test_tp4_branching_shard_two_phases():
+    sc = S.ALL["branching_tp4"]()
+    log(f"case: branching_tp4 seed={sc.seed} Hq={sc.hq} Hkv={sc.hkv}")
+    run = ScenarioRun(sc)
+    inp, oe, _ = run_phase(run, 0)
+    check_extend(run, inp, oe, sample=[0, 63], rows_per_req=16, what="branching_tp4/extend")
+    run.finish(0, inp)
+    inp2, _, od = run_phase(run, 1)
+    check_decode(run, inp2, od, sample=[0, 33, 63], what="branching_tp4/decode")

@@ -240,6 +240,43 @@ def cfg5_mixed_small(seed: int = SEED_BASE + 5) -> Scenario:
     return sc
 
 
+def jump_forward(seed: int = SEED_BASE + 6, n_req: int = 256, ctx=(1024, 8192), ext=(2, 32),
+                 hq: int = 32, hkv: int = 8, pool: int = 2097152) -> Scenario:
+    """Jump-forward extends (the runtime effect of a compressed FSM, section 4):
+    each request's context is a cached path of a random segment tree
+    (L ~ U[ctx]), and it appends a deterministic run of E ~ U{ext} tokens in
+    one extend instead of E decode steps.  GQA 32/8/128."""
+    rng = np.random.default_rng(seed)
+    tree = SegmentTree(seed, 4, 256, 1024)
+    reqs = []
+    for r in range(n_req):
+        p = int(rng.integers(ctx[0], ctx[1] + 1))
+        e = int(rng.integers(ext[0], ext[1] + 1))
+        toks = np.concatenate([tree.random_path_tokens(rng, p), _private(seed, 1, r, e)])
+        reqs.append(ExtendReq(toks, p, e))
+    return Scenario("jump_forward", seed, hq, hkv, 128, pool, 0, _no_history, [Phase(extend=reqs)])
+
+
+def jump_forward_small(seed: int = SEED_BASE + 6) -> Scenario:
+    """Scaled-down jump-forward workload for full oracle comparison."""
+    sc = jump_forward(seed, n_req=12, ctx=(40, 600), ext=(1, 33), pool=16384)
+    sc.name = "jump_forward_small"
+    return sc
+
+
+def tp_shard(base: Callable[[], Scenario], hq: int, hkv: int, name: str) -> Callable[[], Scenario]:
+    """One GPU's share of a tensor-parallel deployment: the same requests and
+    slot tables with hq query heads and hkv kv heads (the head shard; the tree
+    and slot ids are identical on every GPU)."""
+
+    def make() -> Scenario:
+        sc = base()
+        sc.hq, sc.hkv, sc.name = hq, hkv, name
+        return sc
+
+    return make
+
+
 ALL = {
     "decode_tiny": cfg1_decode_tiny,
     "extend_fewshot": cfg2_extend_fewshot,
@@ -247,6 +284,12 @@ ALL = {
     "branching": cfg4_branching,
     "mixed": cfg5_mixed,
     "mixed_small": cfg5_mixed_small,
+    "jump_forward": jump_forward,
+    "jump_forward_small": jump_forward_small,
+    # tensor-parallel head shards: 32/8 heads at TP=4, 64/8 heads at TP=8
+    "decode_chat_tp4": tp_shard(cfg3_decode_chat, 8, 2, "decode_chat_tp4"),
+    "branching_tp4": tp_shard(cfg4_branching, 8, 2, "branching_tp4"),
+    "mixed_tp8": tp_shard(cfg5_mixed, 8, 1, "mixed_tp8"),
 }
 
 
