@@ -162,6 +162,31 @@ def scheduler_report(sc, n: int = 300):
     return out
 
 
+def data_parallel_report(sc, n: int = 2000, n_workers: int = 4):
+    """Appendix A.4 on the workload's own stream: the first n history requests
+    dispatched over n_workers replicas (each with a quarter of a cache sized
+    for about a fifth of the stream's tokens) by the router meta-tree, with
+    the affinity policy and with cache-blind policies; a single cache of the
+    same total size is the bound.  Evictions are committed to the router
+    every 50 requests."""
+    from paper_2312_07104_amd.runtime import run_data_parallel
+
+    seqs = [np.asarray(sc.history(i), dtype=np.int32) for i in range(min(n, sc.history_len))]
+    if not seqs:
+        return None
+    total = sum(len(x) for x in seqs)
+    per_worker = max(max(len(x) for x in seqs), total // (5 * n_workers))
+    t0 = time.perf_counter()
+    single = run_data_parallel(seqs, 1, n_workers * per_worker, "least_loaded")
+    out = {"requests": len(seqs), "prefill_tokens": total, "workers": n_workers, "slots_per_worker": per_worker,
+           "commit_every": 50, "single_cache_hit_rate": single.hit_rate}
+    for policy in ("affinity", "least_loaded", "round_robin", "random"):
+        r = run_data_parallel(seqs, n_workers, per_worker, policy, commit_every=50, seed=1)
+        out[policy] = {"hit_rate": r.hit_rate, "imbalance": r.imbalance, "router_nodes": r.router_nodes}
+    out["seconds"] = time.perf_counter() - t0
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -315,6 +340,7 @@ def main():
                       "plan_batch_ms": run.plan_seconds * 1e3},
     }
     line["scheduler"] = scheduler_report(sc)
+    line["data_parallel"] = data_parallel_report(sc)
     if not args.no_cpu_baseline:
         log("[bench] timing the oracle on host cores")
         line["cpu_baseline"] = cpu_baseline(sc, inp, args.cpu_budget)

@@ -113,6 +113,45 @@ int64_t ra_num_nodes(const ra_cache* c);      /* live nodes, root included */
  * EINVAL if cap is too small. */
 int ra_snapshot(const ra_cache* c, int64_t* buf, int64_t cap, int64_t* out_len);
 
+/* Eviction log, for a router that mirrors this tree (Appendix A.4: workers
+ * commit their evictions to a queue the router applies later).  While
+ * enabled, every leaf ra_evict frees appends one entry: the tokens of its
+ * root-to-leaf path and the leaf's own length (the evicted suffix of that
+ * path).  Disabling drops the pending entries. */
+int ra_cache_log_evictions(ra_cache* c, int32_t enable);
+/* Pops the oldest entry: tokens[0..*out_path_len) = its path,
+ * *out_evicted_len = the evicted suffix length.  An empty log gives
+ * *out_path_len = -1 and RA_OK.  EINVAL if cap < the path length (the entry
+ * stays queued; *out_path_len reports the size needed). */
+int ra_eviction_log_pop(ra_cache* c, int32_t* tokens, int64_t cap, int64_t* out_path_len,
+                        int64_t* out_evicted_len);
+
+/* ===================================================================== */
+/* Host: data-parallel router meta-tree (Appendix A.4).                  */
+/* ===================================================================== */
+
+/* A trie over the token sequences of up to 64 replica workers; every node
+ * records which workers hold its prefix.  Host memory only, not thread-safe
+ * per handle (one router thread).  The view is what the caller reports:
+ * inserts at dispatch, evictions when the caller commits them, so between
+ * commits it may still credit a worker with a prefix it has dropped. */
+typedef struct ra_router ra_router;
+
+int ra_router_create(int32_t n_workers, ra_router** out); /* 1 <= n_workers <= 64 */
+void ra_router_destroy(ra_router* r);
+/* out_len[w] (n_workers entries) = the longest prefix of tokens[0..n) that
+ * worker w holds in the router's view. */
+int ra_router_match(const ra_router* r, const int32_t* tokens, int64_t n, int64_t* out_len);
+/* Records that worker holds tokens[0..n) (splits nodes where needed). */
+int ra_router_insert(ra_router* r, int32_t worker, const int32_t* tokens, int64_t n);
+/* Commits one eviction of the worker: it dropped the last evicted_len tokens
+ * of the path tokens[0..path_len) and everything below them.  Ranges the
+ * router never recorded are ignored.  Nodes no worker holds are freed. */
+int ra_router_evict(ra_router* r, int32_t worker, const int32_t* tokens, int64_t path_len,
+                    int64_t evicted_len);
+int64_t ra_router_num_nodes(const ra_router* r);                   /* live nodes, root included */
+int64_t ra_router_held_tokens(const ra_router* r, int32_t worker); /* -1 for a bad worker */
+
 /* ===================================================================== */
 /* Device: KV pool and attention (gfx950 HIP kernels).                   */
 /* ===================================================================== */

@@ -44,6 +44,15 @@ _SIGS = {
     "ra_cached_tokens": ([_vp], _i64),
     "ra_num_nodes": ([_vp], _i64),
     "ra_snapshot": ([_vp, _vp, _i64, _i64p], ctypes.c_int),
+    "ra_cache_log_evictions": ([_vp, _i32], ctypes.c_int),
+    "ra_eviction_log_pop": ([_vp, _vp, _i64, _i64p, _i64p], ctypes.c_int),
+    "ra_router_create": ([_i32, ctypes.POINTER(_vp)], ctypes.c_int),
+    "ra_router_destroy": ([_vp], None),
+    "ra_router_match": ([_vp, _vp, _i64, _vp], ctypes.c_int),
+    "ra_router_insert": ([_vp, _i32, _vp, _i64], ctypes.c_int),
+    "ra_router_evict": ([_vp, _i32, _vp, _i64, _i64], ctypes.c_int),
+    "ra_router_num_nodes": ([_vp], _i64),
+    "ra_router_held_tokens": ([_vp, _i32], _i64),
     "ra_store_kv": ([_vp, _vp, _vp, _i64, _vp, _vp, _i64, _i32, _i32, _vp], ctypes.c_int),
     "ra_extend_attention": ([_vp, _vp, _vp, _i64, _vp, _vp, _i64, _vp, _i64, _i64, _vp, _vp, _vp, _vp,
                              _i32, _i32, _i32, _i32, _i32, ctypes.c_float, _vp, _vp], ctypes.c_int),
@@ -159,6 +168,22 @@ class RadixCache:
     def num_nodes(self) -> int:
         return _lib.ra_num_nodes(self._h)
 
+    def log_evictions(self, enable: bool = True) -> None:
+        """Start (or stop and clear) the eviction log."""
+        _check(_lib.ra_cache_log_evictions(self._h, 1 if enable else 0))
+
+    def pop_eviction(self):
+        """Oldest logged eviction as (root-to-leaf path tokens, evicted suffix
+        length), or None when the log is empty."""
+        n, k = _i64(), _i64()
+        # size probe: an empty log reports -1; otherwise EINVAL with the size
+        _lib.ra_eviction_log_pop(self._h, None, 0, ctypes.byref(n), ctypes.byref(k))
+        if n.value < 0:
+            return None
+        buf = np.empty(max(n.value, 1), dtype=np.int32)
+        _check(_lib.ra_eviction_log_pop(self._h, buf.ctypes.data, buf.shape[0], ctypes.byref(n), ctypes.byref(k)))
+        return buf[: n.value], k.value
+
     def snapshot(self) -> dict:
         """Same canonical form as the oracle's RadixCache.snapshot()."""
         n = _i64()
@@ -176,6 +201,45 @@ class RadixCache:
             nodes.append((nid, parent, ref, stamp, key, slots))
         free = [int(x) for x in buf[i : i + n_free]]
         return {"nodes": nodes, "free": free, "clock": clock}
+
+
+class Router:
+    """The native data-parallel router meta-tree (which workers hold which
+    prefixes)."""
+
+    def __init__(self, n_workers: int):
+        h = _vp()
+        _check(_lib.ra_router_create(n_workers, ctypes.byref(h)))
+        self._h = h
+        self.n_workers = n_workers
+
+    def __del__(self):
+        h = getattr(self, "_h", None)
+        lib = _lib
+        if h and lib is not None:
+            lib.ra_router_destroy(h)
+            self._h = None
+
+    def match(self, tokens) -> np.ndarray:
+        """Per worker, the longest prefix of tokens it holds (router's view)."""
+        t = _np_i32(tokens)
+        out = np.zeros(self.n_workers, dtype=np.int64)
+        _check(_lib.ra_router_match(self._h, t.ctypes.data, t.shape[0], out.ctypes.data))
+        return out
+
+    def insert(self, worker: int, tokens) -> None:
+        t = _np_i32(tokens)
+        _check(_lib.ra_router_insert(self._h, worker, t.ctypes.data, t.shape[0]))
+
+    def evict(self, worker: int, path, evicted_len: int) -> None:
+        t = _np_i32(path)
+        _check(_lib.ra_router_evict(self._h, worker, t.ctypes.data, t.shape[0], evicted_len))
+
+    def num_nodes(self) -> int:
+        return _lib.ra_router_num_nodes(self._h)
+
+    def held_tokens(self, worker: int) -> int:
+        return _lib.ra_router_held_tokens(self._h, worker)
 
 
 # ---------------------------------------------------------------------------

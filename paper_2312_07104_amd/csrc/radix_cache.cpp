@@ -20,6 +20,7 @@
 #include <algorithm>
 #include <cstdint>
 #include <cstring>
+#include <deque>
 #include <set>
 #include <string>
 #include <unordered_map>
@@ -62,6 +63,15 @@ struct ra_cache {
   int64_t live = 1;
   int64_t evictable = 0;  // tokens in unreferenced live nodes
   int64_t cached = 0;     // tokens in live nodes
+
+  // Optional eviction log (for a data-parallel router that mirrors this
+  // tree): per evicted leaf, its root-to-leaf tokens and its own length.
+  struct Evicted {
+    std::vector<int32_t> path;
+    int64_t len;
+  };
+  bool log_evictions = false;
+  std::deque<Evicted> eviction_log;
 
   bool evictable_leaf(int64_t id) const {
     const Node& n = nodes[id];
@@ -327,6 +337,17 @@ int ra_evict(ra_cache* c, int64_t n_tokens, int64_t* out_freed) {
     c->lru.erase(c->lru.begin());
     Node& n = c->nodes[x];
     n.in_lru = false;
+    if (c->log_evictions) {
+      ra_cache::Evicted e;
+      e.len = static_cast<int64_t>(n.key.size());
+      std::vector<int64_t> chain;
+      for (int64_t y = x; y != 0; y = c->nodes[y].parent) chain.push_back(y);
+      for (auto it = chain.rbegin(); it != chain.rend(); ++it) {
+        const auto& k = c->nodes[*it].key;
+        e.path.insert(e.path.end(), k.begin(), k.end());
+      }
+      c->eviction_log.push_back(std::move(e));
+    }
     for (int32_t s : n.slots) c->push_free(s);
     int64_t len = static_cast<int64_t>(n.key.size());
     freed += len;
@@ -342,6 +363,30 @@ int ra_evict(ra_cache* c, int64_t n_tokens, int64_t* out_freed) {
     c->refresh(par);
   }
   if (out_freed) *out_freed = freed;
+  return ra_ok();
+}
+
+int ra_cache_log_evictions(ra_cache* c, int32_t enable) {
+  if (!c) return ra_fail(RA_EINVAL, "ra_cache_log_evictions: cache is NULL");
+  c->log_evictions = enable != 0;
+  if (!c->log_evictions) c->eviction_log.clear();
+  return ra_ok();
+}
+
+int ra_eviction_log_pop(ra_cache* c, int32_t* tokens, int64_t cap, int64_t* out_path_len, int64_t* out_evicted_len) {
+  if (!c || !out_path_len) return ra_fail(RA_EINVAL, "ra_eviction_log_pop: NULL argument");
+  if (c->eviction_log.empty()) {
+    *out_path_len = -1;
+    if (out_evicted_len) *out_evicted_len = 0;
+    return ra_ok();
+  }
+  const auto& e = c->eviction_log.front();
+  const int64_t n = static_cast<int64_t>(e.path.size());
+  *out_path_len = n;
+  if (out_evicted_len) *out_evicted_len = e.len;
+  if (!tokens || cap < n) return ra_fail(RA_EINVAL, "ra_eviction_log_pop: token buffer too small");
+  std::memcpy(tokens, e.path.data(), sizeof(int32_t) * n);
+  c->eviction_log.pop_front();
   return ra_ok();
 }
 

@@ -294,3 +294,115 @@ def run_offline(sequences, pool_slots: int, policy: str = "lspf", seed: int = 0,
         computed += need
         total += int(seqs[i].shape[0])
     return OfflineResult(order, computed, total)
+
+
+# ---------------------------------------------------------------------------
+# Data parallelism: a router meta-tree over replica workers (Appendix A.4)
+# ---------------------------------------------------------------------------
+
+DP_POLICIES = ("affinity", "least_loaded", "round_robin", "random")
+
+
+@dataclass
+class DataParallelResult:
+    policy: str
+    n_workers: int
+    prefill_tokens: int
+    computed_tokens: int
+    worker_work: list[int]         # computed (prefilled) tokens per worker
+    worker_requests: list[int]
+    router_nodes: int
+
+    @property
+    def hit_rate(self) -> float:
+        return 1.0 - self.computed_tokens / self.prefill_tokens if self.prefill_tokens else 0.0
+
+    @property
+    def imbalance(self) -> float:
+        """Largest worker's work over the mean (1.0 = perfectly balanced)."""
+        mean = sum(self.worker_work) / len(self.worker_work)
+        return max(self.worker_work) / mean if mean else 1.0
+
+
+def _serve(cache: RadixCache, seq: np.ndarray) -> int:
+    """One request on one worker: match, lock, compute (allocate) the rest,
+    evicting when the pool is short (Algorithm 1), insert, unlock.  Returns
+    the number of computed tokens."""
+    node, m, slots = cache.match_prefix(seq)
+    cache.inc_ref(node)
+    need = seq.shape[0] - m
+    if need:
+        try:
+            new = cache.alloc(need)
+        except OutOfSlots:
+            cache.evict(need)
+            new = cache.alloc(need)
+        cache.insert(seq, np.concatenate([slots, new]))
+    cache.dec_ref(node)
+    return need
+
+
+def run_data_parallel(sequences, n_workers: int, pool_slots: int, policy: str = "affinity",
+                      commit_every: int = 1, slack: float = 0.1, seed: int = 0, free_order=None,
+                      probe=None) -> DataParallelResult:
+    """Dispatches a request stream over ``n_workers`` replicas, each with its
+    own radix cache of ``pool_slots`` slots, through the router meta-tree.
+
+    The router records a request's sequence for the chosen worker at dispatch
+    (both sides update their trees independently); workers log their
+    evictions and the router applies the logs every ``commit_every`` requests
+    (its idle periods), so in between its view may be stale.
+
+    Policies: ``affinity`` picks the worker with the longest cached prefix of
+    the prompt (router view) among the workers whose accumulated work is
+    within ``slack`` of the mean plus this request (ties and no match: the
+    least loaded); ``least_loaded``, ``round_robin`` and ``random`` ignore
+    the caches.  ``probe(router, workers)`` is called after every commit
+    (tests check the router against the worker trees there)."""
+    if policy not in DP_POLICIES:
+        raise ValueError(f"unknown policy {policy!r}; one of {DP_POLICIES}")
+    from . import Router
+
+    seqs = [np.ascontiguousarray(s, dtype=np.int32) for s in sequences]
+    router = Router(n_workers)
+    workers = [RadixCache(pool_slots, free_order) for _ in range(n_workers)]
+    for c in workers:
+        c.log_evictions(True)
+    rng = np.random.default_rng(seed)
+    work = [0] * n_workers
+    nreq = [0] * n_workers
+    computed = total = 0
+
+    def commit():
+        for w, c in enumerate(workers):
+            while True:
+                e = c.pop_eviction()
+                if e is None:
+                    break
+                router.evict(w, e[0], e[1])
+        if probe is not None:
+            probe(router, workers)
+
+    for i, seq in enumerate(seqs):
+        n = int(seq.shape[0])
+        if policy == "affinity":
+            m = router.match(seq)
+            mean = sum(work) / n_workers
+            ok = [w for w in range(n_workers) if work[w] <= (1.0 + slack) * mean + n] or list(range(n_workers))
+            w = max(ok, key=lambda x: (int(m[x]), -work[x], -x))
+        elif policy == "least_loaded":
+            w = min(range(n_workers), key=lambda x: (work[x], x))
+        elif policy == "round_robin":
+            w = i % n_workers
+        else:
+            w = int(rng.integers(n_workers))
+        router.insert(w, seq)
+        need = _serve(workers[w], seq)
+        work[w] += need
+        nreq[w] += 1
+        computed += need
+        total += n
+        if (i + 1) % commit_every == 0:
+            commit()
+    commit()
+    return DataParallelResult(policy, n_workers, total, computed, work, nreq, router.num_nodes())
