@@ -40,7 +40,7 @@ FLUSH_BYTES = 1 << 30
 CSRC = os.path.join(ROOT, "paper_2312_07104_amd", "csrc")
 # sources whose code a kernel's launch runs (traffic figures are tied to them)
 KERNEL_SOURCES = {
-    "extend": ["extend.hip", "extend_wide.hip", "lds_dma.h", "device_common.h"],
+    "extend": ["extend.hip", "lds_dma.h", "device_common.h"],
     "decode": ["decode.hip", "lds_dma.h", "device_common.h"],
 }
 

@@ -26,10 +26,10 @@ HIP_ONLY = [f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang", "
             "-mno-amdgpu-ieee", "-fno-honor-nans"]
 
 
-# Per-source extra flags.  extend_wide.hip keeps its S^T MFMAs in VGPR form
-# (the softmax reads them with the VALU) although the kernel also uses AGPRs
-# for the O^T accumulators through inline assembly.
-EXTRA = {"extend_wide.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"]}
+# Per-source extra flags.  extend.hip keeps the compiler's own MFMAs in VGPR
+# form (the prologue's S^T, read by the VALU) although the kernel holds Q^T
+# and the O^T accumulators in AGPRs through inline assembly.
+EXTRA = {"extend.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"]}
 
 
 def _run(cmd):

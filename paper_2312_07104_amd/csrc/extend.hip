@@ -1,33 +1,46 @@
-// Extend attention: prefill of a request's new tokens over its cached prefix
-// (the work that remains once RadixAttention has reused the prefix's KV
-// cache; section 3, Appendix A.1), plus causal attention among the new
-// tokens.  This is a dense contraction, so QK^T and PV run on bf16 MFMA
+// Extend attention (ra_extend_attention): prefill of a request's new tokens
+// over its cached prefix (the work that remains once RadixAttention reuses the
+// prefix's KV cache; section 3, Appendix A.1) plus causal attention among the
+// new tokens.  A dense contraction, so QK^T and PV run on bf16 MFMA
 // (v_mfma_f32_16x16x32_bf16) with fp32 accumulation.
 //
-// Work item = (request, kv head, query tile).  A tile holds 128 query rows
-// packed as (new token, query head of the kv head's group): the G heads that
-// share a kv head share every K/V tile the work-group stages.  Four waves of
-// 32 rows.  Per 64-key tile:
-//   * K and V rows are copied HBM -> LDS by direct-to-LDS loads
-//     (global_load_lds_dwordx4), no VGPR staging.  Prefix keys are gathered
-//     through the request's slot-table row, new keys come from the contiguous
-//     k_new / v_new rows.  The slot indices themselves travel by DMA into a
-//     small LDS ring two tiles ahead, so a tile's gather never waits on its
-//     index load.  The K/V ring has two stages.
-//   * A DMA writes lane i's 16 bytes at base + 16 i, so rows sit unpadded at
-//     2*D bytes; the 16-byte pieces of row r are XOR-swizzled by ra_kv_swz(r) (the
-//     source address picks the piece) to spread LDS banks.
-//   * S^T[key, query] = K Q^T with the queries as the MFMA columns: each lane
-//     owns one query column, so the row max / row sum are in-lane plus two
-//     cross-row shuffles.  K rows are fed to the A operand in the order that
-//     makes the accumulator's four 16-lane row groups hold keys 8g..8g+7 of
-//     each 32-key step, which is exactly P^T's B-operand layout.
-//   * O^T += V^T P^T: V stays row-major in LDS; ds_read_b64_tr_b16 reads it
-//     transposed (lane i of a 16-lane group gets column i of four rows), two
-//     reads per A operand.
-// The DMAs are issued from inline assembly: the compiler would otherwise
-// wait for every outstanding DMA before each LDS read, serialising the
-// pipeline.  Waits are explicit s_waitcnt vmcnt at the top of each tile.
+// Work item = (request, kv head, query tile).  A tile packs query rows as
+// (new token, query head of the kv head's group), so the G heads sharing a kv
+// head share every K/V tile.  Waves of 32 query rows (two 16-column MFMA
+// blocks), two waves per SIMD: eight waves and 256 rows per work-group with
+// 64-key tiles (one work-group per CU), or four waves and 128 rows with
+// 32-key tiles (two per CU) for requests with fewer rows.
+//   * K/V tiles arrive by direct-to-LDS copies (global_load_lds_dwordx4: a
+//     prefix row is gathered through the request's slot-table row, a new
+//     token's row read from k_new / v_new) into a four-stage ring, two tiles
+//     of lead.  The slot indices travel by copy four tiles ahead into their
+//     own ring and are read into registers a tile before use.  Rows use the
+//     ra_kv_swz piece layout (conflict-free operand reads).
+//   * The loop runs over 32-key halves, software pipelined in one issue
+//     order that sched_barrier fences hold: the S^T = K Q^T MFMAs of the next
+//     half, each followed by one probability of the current half (fma +
+//     exp2, bf16 pack every second), then the current half's PV MFMAs with
+//     the next half's maxima between them.  About 1.5 VALU instructions per
+//     MFMA, which one wave can issue under the matrix core's pace.
+//   * At a tile's top (one barrier) the wave computes the addresses of the
+//     copies two tiles ahead; the copies themselves are issued one every two
+//     PV MFMA steps of the next fused step, so the waves never queue their
+//     copies at the address unit all at once.
+//   * Q^T and the O^T accumulators live in AGPRs (inline-assembly MFMAs with
+//     "a" operands); S^T stays in VGPRs, where the softmax reads it.  The
+//     compiler does not track hazards of inline assembly, so the code keeps
+//     the wait states itself: two after the VALU writes P^T, several MFMAs
+//     between an S^T MFMA and the VALU reading its result, and a long s_nop
+//     run before the VALU touches O (rare rescale, epilogue).
+//   * Online softmax in the base-2 domain.  The running maximum moves only
+//     when some score exceeds it by more than 2^24 after exponentiation, so
+//     after the first half of a query tile the rescale path is practically
+//     never taken; the test is on each lane's partial maximum, so the common
+//     path has no cross-lane reduction.  Probabilities up to 2^24 cannot
+//     overflow the fp32 accumulators (2^24 times 2^22 keys times |v|).  Row
+//     sums come from an MFMA against a ones operand, so numerator and
+//     denominator see the same bf16 P.
+
 #include <type_traits>
 
 #include "device_common.h"
@@ -35,37 +48,60 @@
 
 namespace {
 
-constexpr int kBM = 128;  // query rows per work-group
-constexpr int kBN = 64;   // keys per tile
-constexpr int64_t kWideMinRows = 256;  // query rows per kv head from which the 256-row kernel is used
+constexpr int kStages = 4;   // K/V tiles resident in LDS
+constexpr int kRing = 4;     // slot-index ring (tiles)
+constexpr int kQB = 2;       // 16-query column blocks per wave (32 query rows)
+// exp2 argument ceiling of the lazy maximum: p <= 2^kLazyLog2
+constexpr float kLazyLog2 = 24.f;
 
-template <int D>
-__global__ __launch_bounds__(256, 2) void extend_kernel(
+// O^T block += A B on AGPR accumulators (the compiler inserts no wait states
+// for it: callers keep VALU writes of A and B at least two wait states away).
+__device__ __forceinline__ void pv_mfma(f32x4_t& o, const bf16x8_t& a, const bf16x8_t& b) {
+  asm("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0" : "+a"(o) : "v"(a), "v"(b));
+}
+
+// S^T block (+)= K Q^T with the Q^T operand in AGPRs and S^T in VGPRs.  The
+// compiler inserts no wait states for it: VALU reads of S^T must come at
+// least 11 wait states after the last MFMA writing it (callers keep several
+// MFMAs in between, or an s_nop run).
+__device__ __forceinline__ void s_mfma_first(f32x4_t& s, const bf16x8_t& a, const bf16x8_t& qa) {
+  asm("v_mfma_f32_16x16x32_bf16 %0, %1, %2, 0" : "=&v"(s) : "v"(a), "a"(qa));
+}
+__device__ __forceinline__ void s_mfma_acc(f32x4_t& s, const bf16x8_t& a, const bf16x8_t& qa) {
+  asm("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0" : "+v"(s) : "v"(a), "a"(qa));
+}
+
+// WAVES waves of 32 query rows per work-group, BN keys per K/V tile (64:
+// two 32-key halves per tile; 32: one).  <D, 8, 64>: 256 rows, one
+// work-group per CU; <D, 4, 32>: 128 rows, two work-groups per CU (65 KB of
+// LDS each).  Either way two waves share each SIMD.
+template <int D, int WAVES, int BN>
+__global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void extend_kernel(
     const __bf16* __restrict__ q, const __bf16* __restrict__ k_new, const __bf16* __restrict__ v_new,
     int64_t total_tokens, const __bf16* __restrict__ k_pool, const __bf16* __restrict__ v_pool,
     int64_t pool_slots, const int32_t* __restrict__ rtt, int64_t rtt_rows, int64_t rtt_stride,
     const int32_t* __restrict__ req_pool_idx, const int32_t* __restrict__ prefix_lens,
     const int32_t* __restrict__ extend_lens, const int32_t* __restrict__ extend_start, int32_t batch,
     int32_t hkv, int32_t grp, int32_t n_qtiles, float scale_log2, __bf16* __restrict__ out) {
+  constexpr int kWaves = WAVES;
+  constexpr int kBN = BN;
+  constexpr int kBM = 32 * WAVES;             // query rows per work-group
+  static_assert(BN == 32 || BN == 64, "tile of one or two 32-key halves");
   constexpr int KS = D / 32;                  // MFMA k-steps over the head dimension = piece groups
   constexpr int DB = D / 16;                  // 16-row blocks of O^T
   constexpr int GROUP_B = kBN * 64;           // bytes of one piece group of a tile
   constexpr int TILE_B = KS * GROUP_B;        // bytes per K (or V) tile
-  constexpr int LOADS = TILE_B / (256 * 16);  // DMA instructions per wave per tile per tensor
-  constexpr int RING = 4;                     // slot-index ring depth
-  // A wave's DMA lane covers tile rows u0 + it * ROW_STEP (it < LOADS); the
-  // index ring stores row u at word LOADS * (u % ROW_STEP) + u / ROW_STEP so
-  // that a lane's LOADS slot indices are one vector LDS read.
-  constexpr int ROW_STEP = kBN / LOADS;
-  static_assert(LOADS == 2 || LOADS == 4, "index vector width");
-  __shared__ __align__(16) unsigned char kv_lds[2][2][TILE_B];
-  __shared__ __align__(16) int32_t idx_lds[RING][kBN];
+  constexpr int STAGE_B = 2 * TILE_B;         // K tile then V tile
+  constexpr int LOADS = TILE_B / (kWaves * 64 * 16);  // DMA instructions per wave per tile per tensor
+  constexpr int ROW_STEP = kBN / LOADS;       // a DMA lane covers rows u0 + it * ROW_STEP
+  static_assert(LOADS == 1 || LOADS == 2, "index vector width");
+  __shared__ __align__(16) unsigned char kv_lds[kStages * STAGE_B];
+  // one index copy moves 64 words (rows beyond the tile are never read)
+  __shared__ __align__(16) int32_t idx_lds[kRing][64];
 
-  // Work-groups go to the 8 XCDs round-robin (block i -> XCD i % 8).  Items
-  // are ordered (kv head, request, query tile, longest tile first) and each
-  // XCD takes a contiguous eighth of that order, so the work-groups in flight
-  // on one XCD share a kv head and mostly one request: they stream the same
-  // K/V rows and hit that XCD's L2.
+  // Work-groups go to the 8 XCDs round-robin (block i -> XCD i % 8); each XCD
+  // takes a contiguous eighth of the (kv head, request, query tile) order, so
+  // the work-groups on one XCD share K/V rows through its L2.
   const int64_t n_items = static_cast<int64_t>(hkv) * batch * n_qtiles;
   const int64_t per_xcd = (n_items + 7) / 8;
   const int64_t item = static_cast<int64_t>(blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
@@ -92,79 +128,93 @@ __global__ __launch_bounds__(256, 2) void extend_kernel(
   const int n_tiles = (kend + kBN - 1) / kBN;
 
   const int tid = threadIdx.x;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform (SGPR)
   const int lane = tid & 63;
   const int c = lane & 15;
   const int g4 = lane >> 4;
 
   // ---- DMA lane mapping (fixed for the kernel) ----------------------------
-  // instruction ch = it*4 + wave covers row block rb = ch / KS, group pg = ch % KS
+  // instruction ch = it * kWaves + wave covers row block rb = ch / KS, group pg = ch % KS
   int dma_row[LOADS];
   uint32_t dma_lds[LOADS];   // byte offset inside a tile (uniform per wave)
   uint32_t dma_gofs[LOADS];  // byte offset inside the gathered global row
 #pragma unroll
   for (int it = 0; it < LOADS; ++it) {
-    const int ch = it * 4 + wave;
+    const int ch = it * kWaves + wave;
     const int rb = ch / KS, pg = ch % KS;
     const int u = 16 * rb + (lane >> 2);
-    const int qlog = (lane & 3) ^ ra_kv_swz(u);
     dma_row[it] = u;
     dma_lds[it] = pg * GROUP_B + rb * 1024;
-    dma_gofs[it] = static_cast<uint32_t>(g * D * 2 + 16 * (4 * pg + qlog));
+    dma_gofs[it] = static_cast<uint32_t>(g * D * 2 + 16 * (4 * pg + ((lane & 3) ^ ra_kv_swz(u))));
   }
   const uint32_t row_bytes = static_cast<uint32_t>(hkv) * D * 2;
   const unsigned char* kpool_b = reinterpret_cast<const unsigned char*>(k_pool);
   const unsigned char* knew_b = reinterpret_cast<const unsigned char*>(k_new);
-  // V rows sit at the same offsets from their own bases
   const int64_t vpool_delta = reinterpret_cast<const unsigned char*>(v_pool) - kpool_b;
   const int64_t vnew_delta = reinterpret_cast<const unsigned char*>(v_new) - knew_b;
   const uint32_t smax = static_cast<uint32_t>(pool_slots - 1);
-  // per-lane K source addresses of row 0 and per-wave LDS offsets, fixed for
-  // the kernel (integer addresses: the new-token base is rebased by -P rows)
   uint64_t kpool_lane[LOADS], knew_lane[LOADS];
-  uint32_t lds_k[2][LOADS], lds_v[2][LOADS];
 #pragma unroll
   for (int it = 0; it < LOADS; ++it) {
     kpool_lane[it] = reinterpret_cast<uint64_t>(kpool_b) + dma_gofs[it];
     knew_lane[it] = reinterpret_cast<uint64_t>(knew_b) + static_cast<uint64_t>(start - P) * row_bytes + dma_gofs[it];
-#pragma unroll
-    for (int st = 0; st < 2; ++st) {
-      lds_k[st][it] = __builtin_amdgcn_readfirstlane(ra_lds_addr(kv_lds[st][0]) + dma_lds[it]);
-      lds_v[st][it] = __builtin_amdgcn_readfirstlane(ra_lds_addr(kv_lds[st][1]) + dma_lds[it]);
-    }
   }
+  const uint32_t lds_kv0 = ra_lds_addr(kv_lds);
 
-  const int u0 = dma_row[0];  // = dma_row[it] - it * ROW_STEP
-  const int idx_pos = (lane % LOADS) * ROW_STEP + lane / LOADS;  // row whose slot lane's word holds
-  auto issue_idx = [&](int tile) {  // wave 0 only: slot indices of one tile
-    const int kb = tile * kBN;
-    if (wave != 0 || tile >= n_tiles || kb >= P) return;
-    const int pos = kb + idx_pos;
-    ra_dma4(trow + (pos < P ? pos : 0), ra_lds_addr(&idx_lds[tile % RING][0]));
+  // The index ring stores tile row u at word LOADS * (u % ROW_STEP) +
+  // u / ROW_STEP, so a lane's LOADS slot indices are one vector LDS read.
+  const int u0 = dma_row[0];
+  const int idx_pos = (lane % LOADS) * ROW_STEP + lane / LOADS;
+  // Wave 0 copies the slot indices of one tile.  It issues the copy for every
+  // tile (reading row position 0 where the tile has no cached rows) so that
+  // each wave's count of outstanding loads per tile is fixed.
+  auto issue_idx = [&](int tile) {
+    if (wave != 0) return;
+    const int pos = tile * kBN + idx_pos;
+    ra_dma4(trow + (tile < n_tiles && pos < P ? pos : 0), ra_lds_addr(&idx_lds[tile % kRing][0]));
   };
-  auto read_slots = [&](int tile, int32_t (&sl)[LOADS]) {
-    const int32_t* w = &idx_lds[tile % RING][LOADS * u0];
-    if constexpr (LOADS == 4) {
-      const int4 v = *reinterpret_cast<const int4*>(w);
-      sl[0] = v.x, sl[1] = v.y, sl[2] = v.z, sl[3] = v.w;
-    } else {
+  // This lane's LOADS slot indices of a tile, read from the index ring (one
+  // vector LDS read; the values are consumed a tile later).
+  auto read_idx = [&](int tile, int32_t (&sl)[LOADS]) {
+    const int32_t* w = &idx_lds[tile % kRing][LOADS * u0];
+    if constexpr (LOADS == 2) {
       const int2 v = *reinterpret_cast<const int2*>(w);
       sl[0] = v.x, sl[1] = v.y;
+    } else {
+      sl[0] = w[0];
     }
   };
-  auto issue_kv = [&](int tile, int stage) {
-    if (tile >= n_tiles) return;
+  // Copies of one tile's K and V rows into stage tile % kStages: 2 * LOADS
+  // per wave (source address per lane, LDS base per wave), K then V for each
+  // it.  sl = the tile's slot indices (read_idx).  A tile past the last one
+  // gets dummy copies of slot 0's row (one cache line per copy) into its
+  // stage, which no wave reads again, so every tile has the same number of
+  // outstanding loads.
+  struct KvCopies {
+    uint64_t src[2 * LOADS];
+    uint32_t lds[2 * LOADS];
+  };
+  auto prep_kv = [&](int tile, const int32_t (&sl)[LOADS], KvCopies& cp) {
     const int kb = tile * kBN;
-    int32_t sl[LOADS];
-    if (kb < P) read_slots(tile, sl);
-    if (kb + kBN <= P) {
-      // every row of the tile is a cached prefix row: gather through the slots
+    const uint32_t kst = lds_kv0 + (tile % kStages) * STAGE_B;
+#pragma unroll
+    for (int it = 0; it < LOADS; ++it) {
+      cp.lds[2 * it] = kst + dma_lds[it];
+      cp.lds[2 * it + 1] = kst + TILE_B + dma_lds[it];
+    }
+    if (tile >= n_tiles) {
+#pragma unroll
+      for (int it = 0; it < LOADS; ++it) {
+        cp.src[2 * it] = kpool_lane[it];
+        cp.src[2 * it + 1] = kpool_lane[it] + vpool_delta;
+      }
+    } else if (kb + kBN <= P) {
 #pragma unroll
       for (int it = 0; it < LOADS; ++it) {
         const uint32_t slot = min(static_cast<uint32_t>(sl[it]), smax);  // negative -> clamped
         const uint64_t src = kpool_lane[it] + static_cast<uint64_t>(slot) * row_bytes;
-        ra_dma16(reinterpret_cast<const void*>(src), lds_k[stage][it]);
-        ra_dma16(reinterpret_cast<const void*>(src + vpool_delta), lds_v[stage][it]);
+        cp.src[2 * it] = src;
+        cp.src[2 * it + 1] = src + vpool_delta;
       }
     } else {
 #pragma unroll
@@ -180,21 +230,46 @@ __global__ __launch_bounds__(256, 2) void extend_kernel(
           src = knew_lane[it] + static_cast<uint64_t>(pos) * row_bytes;
           vdelta = vnew_delta;
         }
-        ra_dma16(reinterpret_cast<const void*>(src), lds_k[stage][it]);
-        ra_dma16(reinterpret_cast<const void*>(src + vdelta), lds_v[stage][it]);
+        cp.src[2 * it] = src;
+        cp.src[2 * it + 1] = src + vdelta;
       }
     }
   };
-
-  // Q^T operands for the wave's two 16-query column blocks (loaded before
-  // the first DMA so that the compiler's wait for these loads does not also
-  // wait for the prologue's DMAs).
-  bf16x8_t qT[2][KS];
-  int qlim[2];  // last key position each of this lane's query columns may see
-  bool qok[2];
-  int64_t qrow[2];
+  auto issue_copy = [&](const KvCopies& cp, int i) {
+    ra_dma16(reinterpret_cast<const void*>(cp.src[i]), cp.lds[i]);
+  };
+  // Top of tile u: K/V(u) is in LDS for every wave and stage (u + 2) %
+  // kStages = (u - 2) % kStages is free.  Order of this wave's loads issued
+  // since the top of u - 1: idx(u + 3) (wave 0 only), then the copies of
+  // K/V(u + 1); the wait retires everything before those, so idx(u + 3) and
+  // K/V(u) have landed, and the barrier makes them visible to all waves.
+  // Then: the index copy of tile u + 4 (into the ring slot of tile u, whose
+  // indices were read at the top of u - 3), the read of tile u + 3's indices
+  // into registers (used at the top of u + 1, so no wait on it here), and the
+  // addresses of tile u + 2's copies from the indices read at the top of
+  // u - 1.  The copies themselves are issued by the next fused step, spread
+  // over its PV MFMAs, so the eight waves do not queue their copies at the
+  // address unit all at once after the barrier.
+  int32_t sl_next[LOADS];  // slot indices of the tile whose copies are prepared next
+  KvCopies cp;
+  auto tile_top = [&](int u) {
+    ra_wait_vmcnt<2 * LOADS>();
+    __builtin_amdgcn_s_barrier();
+    issue_idx(u + 4);
+    int32_t sl[LOADS];
 #pragma unroll
-  for (int j = 0; j < 2; ++j) {
+    for (int it = 0; it < LOADS; ++it) sl[it] = sl_next[it];
+    read_idx(u + 3, sl_next);
+    prep_kv(u + 2, sl, cp);
+  };
+
+  // Q^T operands of the wave's four 16-query column blocks.
+  bf16x8_t qT[kQB][KS];
+  int qlim[kQB];  // last key position each of this lane's query columns may see
+  bool qok[kQB];
+  int64_t qrow[kQB];
+#pragma unroll
+  for (int j = 0; j < kQB; ++j) {
     const int m = 32 * wave + 16 * j + c;
     const int it = tok0 + m / grp;
     qok[j] = it < tok_end;
@@ -202,30 +277,45 @@ __global__ __launch_bounds__(256, 2) void extend_kernel(
     qrow[j] = (start + min(it, tok_end - 1)) * hq + g * grp + m % grp;
     const __bf16* qp = q + qrow[j] * D + 8 * g4;
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks)
-      qT[j][ks] = __builtin_bit_cast(bf16x8_t, qok[j] ? ra_ld16(qp + 32 * ks) : make_uint4(0, 0, 0, 0));
+    for (int ks = 0; ks < KS; ++ks) qT[j][ks] = __builtin_bit_cast(bf16x8_t, ra_ld16(qp + 32 * ks));
   }
 
-  // ---- prologue: indices for tiles 0 and 1, K/V for tile 0 ----------------
-  issue_idx(0);
-  issue_idx(1);
+  // ---- prologue ------------------------------------------------------------
+#pragma unroll
+  for (int t = 0; t < kRing; ++t) issue_idx(t);
   ra_wait_vmcnt<0>();
   __syncthreads();
-  issue_kv(0, 0);
-
-  // O^T accumulators; block DB holds the row sums (A operand = ones), so the
-  // softmax denominator comes from the same bf16 P as the numerator.
-  f32x4_t o[DB + 1][2];
+  {
+    int32_t sl0[LOADS], sl1[LOADS];
+    read_idx(0, sl0);
+    read_idx(1, sl1);
+    read_idx(2, sl_next);
+    prep_kv(0, sl0, cp);
 #pragma unroll
-  for (int i = 0; i <= DB; ++i) o[i][0] = o[i][1] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  float m_run[2] = {-INFINITY, -INFINITY};  // raw score units
-  const uint4 ones_w = make_uint4(0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u);
-  const bf16x8_t ones = __builtin_bit_cast(bf16x8_t, ones_w);
+    for (int i = 0; i < 2 * LOADS; ++i) issue_copy(cp, i);
+    prep_kv(1, sl1, cp);
+#pragma unroll
+    for (int i = 0; i < 2 * LOADS; ++i) issue_copy(cp, i);
+  }
 
-  // Per-lane LDS offsets.  S^T block bb of 32-key step k2 feeds A-operand row
-  // c with key r = 32 k2 + 4 bb + r0, r0 = 8 (c >> 2) + (c & 3), so that the
-  // accumulator's row group g4 holds keys 8 g4 .. 8 g4 + 7 of the step:
-  // P^T's B-operand k slots in natural order.
+  f32x4_t o[DB + 1][kQB];  // O^T blocks; block DB holds the row sums (A operand = ones)
+#pragma unroll
+  for (int i = 0; i <= DB; ++i)
+#pragma unroll
+    for (int j = 0; j < kQB; ++j) o[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  float m_run[kQB], thr[kQB], mb[kQB];  // running max (raw units), its lazy threshold, -m * scale_log2
+#pragma unroll
+  for (int j = 0; j < kQB; ++j) m_run[j] = thr[j] = -INFINITY, mb[j] = 0.f;
+  const float lazy_raw = kLazyLog2 / scale_log2;
+  // A operand of the row-sum MFMA.  It passes through the P^T wait-state asm
+  // below on every half, so the compiler cannot rematerialise it with a VALU
+  // move right in front of the MFMA.
+  bf16x8_t ones = __builtin_bit_cast(bf16x8_t, make_uint4(0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u));
+
+  // Per-lane LDS offsets.  S^T block bb of half k2 feeds A-operand row c with
+  // key r = 32 k2 + 4 bb + r0, r0 = 8 (c >> 2) + (c & 3): the accumulator's
+  // row group g4 then holds keys 8 g4 .. 8 g4 + 7 of the half, P^T's
+  // B-operand k slots in natural order.
   const int r0 = 8 * (c >> 2) + (c & 3);
   const uint32_t koff = r0 * 64 + 16 * (g4 ^ ra_kv_swz(r0));
   // V^T via transposed reads: lane supplies row 32 k2 + 4 h + (8 g4 + (c >> 2))
@@ -235,105 +325,292 @@ __global__ __launch_bounds__(256, 2) void extend_kernel(
 #pragma unroll
   for (int e = 0; e < 2; ++e) voff[e] = vr * 64 + 16 * ((2 * e + ((c & 3) >> 1)) ^ ra_kv_swz(vr)) + 8 * (c & 1);
 
-  auto tile = [&](auto stage_tag, int t) {
-    constexpr int ST = decltype(stage_tag)::value;
-    const int kbase = t * kBN;
-    ra_wait_vmcnt<0>();
-    __syncthreads();
-    issue_idx(t + 2);
-    issue_kv(t + 1, ST ^ 1);
-
-    const unsigned char* kst = kv_lds[ST][0];
-    const unsigned char* vst = kv_lds[ST][1];
-
-    f32x4_t sacc[2][2][2];  // [k2][bb][query block]
+  // S^T of one 32-key half: s[bb][j], element i = key 32 k2 + 8 g4 + 4 bb + i.
+  // (Prologue only; the main loop computes S^T inside the fused step.)
+  auto compute_s = [&](f32x4_t (&s)[2][kQB], int tile, int k2) {
+    const unsigned char* kst = kv_lds + (tile % kStages) * STAGE_B;
 #pragma unroll
-    for (int k2 = 0; k2 < 2; ++k2)
+    for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
       for (int bb = 0; bb < 2; ++bb) {
-        sacc[k2][bb][0] = sacc[k2][bb][1] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        const bf16x8_t a = __builtin_bit_cast(
+            bf16x8_t, *reinterpret_cast<const uint4*>(kst + koff + ks * GROUP_B + (32 * k2 + 4 * bb) * 64));
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-          const bf16x8_t a = __builtin_bit_cast(
-              bf16x8_t, *reinterpret_cast<const uint4*>(kst + koff + ks * GROUP_B + (32 * k2 + 4 * bb) * 64));
-          sacc[k2][bb][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qT[0][ks], sacc[k2][bb][0], 0, 0, 0);
-          sacc[k2][bb][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qT[1][ks], sacc[k2][bb][1], 0, 0, 0);
+        for (int j = 0; j < kQB; ++j) {
+          if (ks == 0) s_mfma_first(s[bb][j], a, qT[j][ks]);
+          else s_mfma_acc(s[bb][j], a, qT[j][ks]);
         }
       }
-    // Element (k2, bb, i) is key kbase + 32 k2 + 8 g4 + 4 bb + i.  Online
-    // softmax in the base-2 domain with a lazily moved maximum: it only moves
-    // when some column's tile maximum exceeds it by more than 2^8 after
-    // scaling, so most tiles skip the rescale; exponentials stay <= 2^8.
-    const bool need_mask = kbase + kBN - 1 > P + tok0;
-    bf16x8_t pT[2][2];  // [k2][query block]
+    // let the last MFMAs retire before the VALU reads S^T
+    asm volatile("s_nop 7\n\ts_nop 7" : "+v"(s[0][0]), "+v"(s[1][kQB - 1]));
+  };
+
+  // Maximum of one half's scores per query column (this lane's 8 keys).
+  auto half_max = [&](f32x4_t (&s)[2][kQB], int j) {
+    float m = __builtin_fmaxf(__builtin_fmaxf(s[0][j][0], s[0][j][1]), s[0][j][2]);
+    m = __builtin_fmaxf(__builtin_fmaxf(m, s[0][j][3]), s[1][j][0]);
+    m = __builtin_fmaxf(__builtin_fmaxf(m, s[1][j][1]), s[1][j][2]);
+    return __builtin_fmaxf(m, s[1][j][3]);
+  };
+
+  // After a half's S^T is complete and its per-lane maxima mt are known:
+  // causal mask (diagonal halves only, maxima recomputed), then the rare move
+  // of the running maximum with its rescale of O^T.
+  auto pre = [&](f32x4_t (&s)[2][kQB], int tile, int k2, float (&mt)[kQB]) {
+    const int kh = tile * kBN + 32 * k2;  // first key of the half
+    if (kh + 31 > P + tok0) {
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      if (need_mask) {
-#pragma unroll
-        for (int k2 = 0; k2 < 2; ++k2)
-#pragma unroll
-          for (int bb = 0; bb < 2; ++bb)
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-              if (kbase + 32 * k2 + 8 * g4 + 4 * bb + i > qlim[j]) sacc[k2][bb][j][i] = -INFINITY;
-      }
-      float mt = -INFINITY;
-#pragma unroll
-      for (int k2 = 0; k2 < 2; ++k2)
-#pragma unroll
-        for (int bb = 0; bb < 2; ++bb)
-          mt = fmaxf(mt, fmaxf(fmaxf(sacc[k2][bb][j][0], sacc[k2][bb][j][1]),
-                               fmaxf(sacc[k2][bb][j][2], sacc[k2][bb][j][3])));
-      mt = ra_max_across_rows(mt);
-      if (__builtin_amdgcn_ballot_w64((mt - m_run[j]) * scale_log2 > 8.f) != 0) {
-        const float m_new = fmaxf(m_run[j], mt);
-        const float alpha = ra_exp2((m_run[j] - m_new) * scale_log2);
-#pragma unroll
-        for (int db = 0; db <= DB; ++db) o[db][j] *= alpha;
-        m_run[j] = m_new;
-      }
-      const float mb = -m_run[j] * scale_log2;
-#pragma unroll
-      for (int k2 = 0; k2 < 2; ++k2) {
-        float p[8];
+      for (int j = 0; j < kQB; ++j) {
 #pragma unroll
         for (int bb = 0; bb < 2; ++bb)
 #pragma unroll
-          for (int i = 0; i < 4; ++i) p[4 * bb + i] = ra_exp2(__builtin_fmaf(sacc[k2][bb][j][i], scale_log2, mb));
-        uint4 w;
-        w.x = ra_pack_bf16x2(p[0], p[1]);
-        w.y = ra_pack_bf16x2(p[2], p[3]);
-        w.z = ra_pack_bf16x2(p[4], p[5]);
-        w.w = ra_pack_bf16x2(p[6], p[7]);
-        pT[k2][j] = __builtin_bit_cast(bf16x8_t, w);
+          for (int i = 0; i < 4; ++i)
+            if (kh + 8 * g4 + 4 * bb + i > qlim[j]) s[bb][j][i] = -INFINITY;
+        mt[j] = half_max(s, j);
       }
     }
-    // O^T += V^T P^T and the row sums += 1 P^T.
+    bool up = false;
 #pragma unroll
-    for (int k2 = 0; k2 < 2; ++k2) {
+    for (int j = 0; j < kQB; ++j) up |= mt[j] > thr[j];
+    if (__builtin_amdgcn_ballot_w64(up) != 0) {
+      // Rare: some column's maximum passed its threshold.  Move those
+      // columns' maxima and rescale their O^T.  The nops give the last
+      // MFMAs that wrote O time to retire before the VALU reads the AGPRs.
 #pragma unroll
-      for (int db = 0; db < DB; ++db) {
-        const unsigned char* vb = vst + voff[db & 1] + (db >> 1) * GROUP_B + 32 * k2 * 64;
-        const bf16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
-            (__attribute__((address_space(3))) bf16x4_t*)(vb));
-        const bf16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
-            (__attribute__((address_space(3))) bf16x4_t*)(vb + 4 * 64));
-        const bf16x8_t a = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-        o[db][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pT[k2][0], o[db][0], 0, 0, 0);
-        o[db][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pT[k2][1], o[db][1], 0, 0, 0);
+      for (int j = 0; j < kQB; ++j) {
+        const float mc = ra_max_across_rows(mt[j]);
+        float alpha = 1.f;
+        if (mc > thr[j]) {
+          alpha = ra_exp2((m_run[j] - mc) * scale_log2);  // 0 while m_run = -inf (O is still 0)
+          m_run[j] = mc;
+          thr[j] = mc + lazy_raw;
+          mb[j] = -mc * scale_log2;
+        }
+        if constexpr (DB == 8) {
+          asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 3"
+                       : "+a"(o[0][j]), "+a"(o[1][j]), "+a"(o[2][j]), "+a"(o[3][j]), "+a"(o[4][j]),
+                         "+a"(o[5][j]), "+a"(o[6][j]), "+a"(o[7][j]), "+a"(o[8][j]));
+        } else {
+          asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 3"
+                       : "+a"(o[0][j]), "+a"(o[1][j]), "+a"(o[2][j]), "+a"(o[3][j]), "+a"(o[4][j]));
+        }
+#pragma unroll
+        for (int db = 0; db <= DB; ++db) o[db][j] *= alpha;
+        // two wait states between the VALU writes of O and the next MFMA
+        if constexpr (DB == 8) {
+          asm volatile("s_nop 1"
+                       : "+a"(o[0][j]), "+a"(o[1][j]), "+a"(o[2][j]), "+a"(o[3][j]), "+a"(o[4][j]),
+                         "+a"(o[5][j]), "+a"(o[6][j]), "+a"(o[7][j]), "+a"(o[8][j]));
+        } else {
+          asm volatile("s_nop 1" : "+a"(o[0][j]), "+a"(o[1][j]), "+a"(o[2][j]), "+a"(o[3][j]), "+a"(o[4][j]));
+        }
       }
-      o[DB][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pT[k2][0], o[DB][0], 0, 0, 0);
-      o[DB][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pT[k2][1], o[DB][1], 0, 0, 0);
     }
   };
 
-  for (int t = 0; t < n_tiles; t += 2) {
-    tile(std::integral_constant<int, 0>{}, t);
-    if (t + 1 < n_tiles) tile(std::integral_constant<int, 1>{}, t + 1);
+  // One software-pipelined step over two halves, written in issue order:
+  // the S^T MFMAs of the next half sn, each followed by one probability of
+  // the current half sc (fma + exp, pack every second), with the K operand
+  // reads two k-steps ahead and the V^T reads of the current half in the
+  // second part; then the current half's PV MFMAs (AGPR accumulators, inline
+  // assembly), the next half's per-lane maxima slotted between them.
+  // sched_barrier(0) fences keep the scheduler from regrouping the MFMAs and
+  // the VALU work, so the matrix core stays busy while the exponentials issue.
+  // HAS_NEXT = false is the last half of the item (no S^T to compute).
+  // kpre holds the K operands of sn's first two k-steps (read by the previous
+  // step); at the end of the PV part the step reads those of the half after
+  // sn, (tile_f, k2_f), when pf is set (its tile is resident by then).
+  constexpr int KP = KS > 1 ? 2 : 1;  // k-steps prefetched across steps
+  // with_copies: issue the copies prepared by the last tile_top, one every
+  // DB / (2 LOADS) PV steps.
+  auto fused = [&](auto has_next, auto with_copies, f32x4_t (&sn)[2][kQB], int tile_n, int k2_n,
+                   f32x4_t (&sc)[2][kQB], int tile_c, int k2_c, float (&mt)[kQB], bf16x8_t (&kpre)[KP][2], bool pf,
+                   int tile_f, int k2_f) {
+    constexpr bool HAS_NEXT = decltype(has_next)::value;
+    constexpr bool COPIES = decltype(with_copies)::value;
+    constexpr int CSTEP = DB / (2 * LOADS) > 0 ? DB / (2 * LOADS) : 1;
+    constexpr int NS = 2 * KS * kQB;  // S^T MFMAs of one half
+    constexpr int NP = 8 * kQB;       // probabilities per lane per half
+    constexpr int VA = 3;             // V^T operands (16-row blocks) read ahead of their PV step
+    const unsigned char* kst = kv_lds + (tile_n % kStages) * STAGE_B + koff + 32 * k2_n * 64;
+    const unsigned char* vst = kv_lds + (tile_c % kStages) * STAGE_B + TILE_B + 32 * k2_c * 64;
+    bf16x8_t kf[KS][2];
+    bf16x4_t vf[DB][2];
+    float p[NP];
+    uint32_t pw[NP / 2];
+    auto read_k = [&](int ks) {
+#pragma unroll
+      for (int bb = 0; bb < 2; ++bb)
+        kf[ks][bb] = __builtin_bit_cast(bf16x8_t,
+                                        *reinterpret_cast<const uint4*>(kst + ks * GROUP_B + 4 * bb * 64));
+    };
+    auto read_v = [&](int db) {
+      const unsigned char* vb = vst + voff[db & 1] + (db >> 1) * GROUP_B;
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+        vf[db][h] =
+            __builtin_amdgcn_ds_read_tr16_b64_v4bf16((__attribute__((address_space(3))) bf16x4_t*)(vb + h * 4 * 64));
+    };
+    auto prob = [&](int v) {  // v = 8 j + 4 bb + i
+      const int j = v >> 3, bb = (v >> 2) & 1, i = v & 3;
+      p[v] = ra_exp2(__builtin_fmaf(sc[bb][j][i], scale_log2, mb[j]));
+      if (v & 1) pw[v >> 1] = ra_pack_bf16x2(p[v - 1], p[v]);
+    };
+    if constexpr (HAS_NEXT) {
+#pragma unroll
+      for (int ks = 0; ks < KP; ++ks)
+#pragma unroll
+        for (int bb = 0; bb < 2; ++bb) kf[ks][bb] = kpre[ks][bb];
+      __builtin_amdgcn_sched_barrier(0);
+      constexpr int PPG = (NP + NS - 1) / NS;  // probabilities per S^T MFMA
+#pragma unroll
+      for (int n = 0; n < NS; ++n) {
+        const int ks = n / (2 * kQB), bb = (n / kQB) & 1, j = n % kQB;
+        if (ks == 0) s_mfma_first(sn[bb][j], kf[ks][bb], qT[j][ks]);
+        else s_mfma_acc(sn[bb][j], kf[ks][bb], qT[j][ks]);
+#pragma unroll
+        for (int v = n * PPG; v < (n + 1) * PPG && v < NP; ++v) prob(v);
+        if (n % (2 * kQB) == 2 * kQB - 1 && ks + 2 < KS) read_k(ks + 2);
+        // the first V^T operands, spread over the last S^T MFMAs
+        if (n >= NS - VA && n - (NS - VA) < DB) read_v(n - (NS - VA));
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    } else {
+#pragma unroll
+      for (int db = 0; db < VA && db < DB; ++db) read_v(db);
+#pragma unroll
+      for (int v = 0; v < NP; ++v) prob(v);
+    }
+    bf16x8_t pT[kQB];
+#pragma unroll
+    for (int j = 0; j < kQB; ++j)
+      pT[j] = __builtin_bit_cast(bf16x8_t, make_uint4(pw[4 * j], pw[4 * j + 1], pw[4 * j + 2], pw[4 * j + 3]));
+    // two wait states between the VALU writes of P^T and the MFMAs reading it
+    asm volatile("s_nop 1" : "+v"(pT[0]), "+v"(pT[1]), "+v"(ones));
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+      if (db + VA < DB) read_v(db + VA);
+      const bf16x8_t a = __builtin_shufflevector(vf[db][0], vf[db][1], 0, 1, 2, 3, 4, 5, 6, 7);
+#pragma unroll
+      for (int j = 0; j < kQB; ++j) pv_mfma(o[db][j], a, pT[j]);
+      // the next half's maxima, one column per PV step once its S^T has retired
+      if constexpr (HAS_NEXT) {
+        if (db >= 2 && db - 2 < kQB) mt[db - 2] = half_max(sn, db - 2);
+      }
+      if constexpr (COPIES) {
+        if (db % CSTEP == CSTEP - 1 && db / CSTEP < 2 * LOADS) issue_copy(cp, db / CSTEP);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+#pragma unroll
+    for (int j = 0; j < kQB; ++j) pv_mfma(o[DB][j], ones, pT[j]);
+    if constexpr (COPIES) {
+#pragma unroll
+      for (int i = DB / CSTEP; i < 2 * LOADS; ++i) issue_copy(cp, i);
+    }
+    if (pf) {
+      const unsigned char* kf_st = kv_lds + (tile_f % kStages) * STAGE_B + koff + 32 * k2_f * 64;
+#pragma unroll
+      for (int ks = 0; ks < KP; ++ks)
+#pragma unroll
+        for (int bb = 0; bb < 2; ++bb)
+          kpre[ks][bb] = __builtin_bit_cast(bf16x8_t,
+                                            *reinterpret_cast<const uint4*>(kf_st + ks * GROUP_B + 4 * bb * 64));
+    }
+    if constexpr (HAS_NEXT) {
+      if constexpr (DB - 2 < kQB) {
+#pragma unroll
+        for (int j = (DB - 2 > 0 ? DB - 2 : 0); j < kQB; ++j) mt[j] = half_max(sn, j);
+      }
+    }
+  };
+
+  // ---- main loop: half h's exponentials and PV run beside half h+1's S^T ---
+  // Every wave takes the tile barrier at the top of its iteration.  The K
+  // operands of each step's first two k-steps were read at the end of the
+  // step before (for the first half of tile t + 1 that read comes after the
+  // barrier of the top of t + 1, so the tile is resident).
+  using yes = std::integral_constant<bool, true>;
+  using no = std::integral_constant<bool, false>;
+  f32x4_t sa[2][kQB], sb[2][kQB];
+  float mt[kQB];
+  bf16x8_t kpre[KP][2];
+  tile_top(0);
+#pragma unroll
+  for (int i = 0; i < 2 * LOADS; ++i) issue_copy(cp, i);
+  compute_s(sa, 0, 0);
+#pragma unroll
+  for (int j = 0; j < kQB; ++j) mt[j] = half_max(sa, j);
+  // K operands of the first two k-steps of a half, read ahead of its step
+  auto load_kpre = [&](int tile, int k2) {
+    const unsigned char* kf_st = kv_lds + (tile % kStages) * STAGE_B + koff + 32 * k2 * 64;
+#pragma unroll
+    for (int ks = 0; ks < KP; ++ks)
+#pragma unroll
+      for (int bb = 0; bb < 2; ++bb)
+        kpre[ks][bb] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const uint4*>(kf_st + ks * GROUP_B + 4 * bb * 64));
+  };
+  if constexpr (BN == 64) load_kpre(0, 1);
+  pre(sa, 0, 0, mt);
+  // The last tile is peeled off the loop so that no branch inside it has two
+  // sides computing the same probabilities (the compiler would hoist them out
+  // of the fused step).
+  if constexpr (BN == 64) {
+    int t = 0;
+    for (; t + 1 < n_tiles; ++t) {
+      tile_top(t + 1);
+      fused(yes{}, yes{}, sb, t, 1, sa, t, 0, mt, kpre, true, t + 1, 0);
+      pre(sb, t, 1, mt);
+      fused(yes{}, no{}, sa, t + 1, 0, sb, t, 1, mt, kpre, true, t + 1, 1);
+      pre(sa, t + 1, 0, mt);
+    }
+    fused(yes{}, no{}, sb, t, 1, sa, t, 0, mt, kpre, false, 0, 0);
+    pre(sb, t, 1, mt);
+    fused(no{}, no{}, sa, 0, 0, sb, t, 1, mt, kpre, false, 0, 0);
+  } else {
+    // One half per tile: the step of tile t + 1 follows that tile's barrier
+    // (its K operands are read there); two tiles per iteration so the S^T
+    // buffers alternate without copies.
+    int t = 0;
+    for (; t + 2 < n_tiles; t += 2) {
+      tile_top(t + 1);
+      load_kpre(t + 1, 0);
+      fused(yes{}, yes{}, sb, t + 1, 0, sa, t, 0, mt, kpre, false, 0, 0);
+      pre(sb, t + 1, 0, mt);
+      tile_top(t + 2);
+      load_kpre(t + 2, 0);
+      fused(yes{}, yes{}, sa, t + 2, 0, sb, t + 1, 0, mt, kpre, false, 0, 0);
+      pre(sa, t + 2, 0, mt);
+    }
+    if (t + 1 < n_tiles) {
+      tile_top(t + 1);
+      load_kpre(t + 1, 0);
+      fused(yes{}, yes{}, sb, t + 1, 0, sa, t, 0, mt, kpre, false, 0, 0);
+      pre(sb, t + 1, 0, mt);
+      fused(no{}, no{}, sa, 0, 0, sb, t + 1, 0, mt, kpre, false, 0, 0);
+    } else {
+      fused(no{}, no{}, sb, 0, 0, sa, t, 0, mt, kpre, false, 0, 0);
+    }
   }
 
+  // No copy may still be landing in LDS once the work-group ends (the last
+  // index copies were issued past the final tile).
+  ra_wait_vmcnt<0>();
+  // Epilogue: let the last MFMAs retire, then normalise by the row sums.
 #pragma unroll
-  for (int j = 0; j < 2; ++j) {
+  for (int j = 0; j < kQB; ++j) {
+    if constexpr (DB == 8) {
+      asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 3"
+                   : "+a"(o[0][j]), "+a"(o[1][j]), "+a"(o[2][j]), "+a"(o[3][j]), "+a"(o[4][j]), "+a"(o[5][j]),
+                     "+a"(o[6][j]), "+a"(o[7][j]), "+a"(o[8][j]));
+    } else {
+      asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 3"
+                   : "+a"(o[0][j]), "+a"(o[1][j]), "+a"(o[2][j]), "+a"(o[3][j]), "+a"(o[4][j]));
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < kQB; ++j) {
     if (!qok[j]) continue;
     const float inv = 1.f / o[DB][j][0];
     __bf16* op = out + qrow[j] * D + 4 * g4;
@@ -347,18 +624,54 @@ __global__ __launch_bounds__(256, 2) void extend_kernel(
   }
 }
 
-template <int D>
-void launch(int64_t items, hipStream_t stream, const __bf16* qp, const __bf16* knp, const __bf16* vnp,
-            int64_t total_tokens, const __bf16* kp, const __bf16* vp, int64_t pool_slots, const int32_t* rtt,
-            int64_t rtt_rows, int64_t rtt_stride, const int32_t* rpi, const int32_t* pl, const int32_t* el,
-            const int32_t* es, int32_t batch, int32_t hkv, int32_t grp, int32_t n_qtiles, float scale_log2,
-            __bf16* op) {
-  hipLaunchKernelGGL((extend_kernel<D>), dim3(static_cast<uint32_t>(items)), dim3(256), 0, stream, qp, knp, vnp,
-                     total_tokens, kp, vp, pool_slots, rtt, rtt_rows, rtt_stride, rpi, pl, el, es, batch, hkv, grp,
-                     n_qtiles, scale_log2, op);
+template <int D, int WAVES, int BN>
+void launch_wide(int64_t items, hipStream_t stream, const __bf16* qp, const __bf16* knp, const __bf16* vnp,
+                 int64_t total_tokens, const __bf16* kp, const __bf16* vp, int64_t pool_slots, const int32_t* rtt,
+                 int64_t rtt_rows, int64_t rtt_stride, const int32_t* rpi, const int32_t* pl, const int32_t* el,
+                 const int32_t* es, int32_t batch, int32_t hkv, int32_t grp, int32_t n_qtiles, float scale_log2,
+                 __bf16* op) {
+  hipLaunchKernelGGL((extend_kernel<D, WAVES, BN>), dim3(static_cast<uint32_t>(items)), dim3(WAVES * 64), 0,
+                     stream, qp, knp, vnp, total_tokens, kp, vp, pool_slots, rtt, rtt_rows, rtt_stride, rpi, pl, el,
+                     es, batch, hkv, grp, n_qtiles, scale_log2, op);
 }
 
 }  // namespace
+
+// Launches the fused-step kernel with 256 (rows = 256) or 128 query rows per
+// work-group for arguments ra_extend_validate accepted.
+static int extend_launch(const void* q, const void* k_new, const void* v_new, int64_t total_tokens,
+                          const void* k_pool, const void* v_pool, int64_t pool_slots, const int32_t* req_to_token,
+                          int64_t rtt_rows, int64_t rtt_stride, const int32_t* req_pool_idx,
+                          const int32_t* prefix_lens, const int32_t* extend_lens, const int32_t* extend_start,
+                          int32_t batch, int32_t max_extend_len, int32_t hq, int32_t hkv, int32_t d, float scale,
+                          void* out, int32_t rows, hipStream_t stream) {
+  const int32_t grp = hq / hkv;
+  const int32_t tpb = (rows == 256 ? 256 : 128) / grp;
+  const int64_t n_qtiles = (static_cast<int64_t>(max_extend_len) + tpb - 1) / tpb;
+  const int64_t items = (static_cast<int64_t>(batch) * hkv * n_qtiles + 7) / 8 * 8;  // whole XCD rounds
+  if (items > INT32_MAX) return ra_fail(RA_EINVAL, "ra_extend_attention: too many work items");
+  const float scale_log2 = scale * RA_LOG2E;
+  auto* qp = static_cast<const __bf16*>(q);
+  auto* knp = static_cast<const __bf16*>(k_new);
+  auto* vnp = static_cast<const __bf16*>(v_new);
+  auto* kp = static_cast<const __bf16*>(k_pool);
+  auto* vp = static_cast<const __bf16*>(v_pool);
+  auto* op = static_cast<__bf16*>(out);
+  const int32_t nq = static_cast<int32_t>(n_qtiles);
+#define RA_WIDE_LAUNCH(DD, W, B)                                                                                   \
+  launch_wide<DD, W, B>(items, stream, qp, knp, vnp, total_tokens, kp, vp, pool_slots, req_to_token, rtt_rows,     \
+                        rtt_stride, req_pool_idx, prefix_lens, extend_lens, extend_start, batch, hkv, grp, nq,    \
+                        scale_log2, op)
+  if (rows == 256) {
+    if (d == 128) RA_WIDE_LAUNCH(128, 8, 64);
+    else RA_WIDE_LAUNCH(64, 8, 64);
+  } else {
+    if (d == 128) RA_WIDE_LAUNCH(128, 4, 32);
+    else RA_WIDE_LAUNCH(64, 4, 32);
+  }
+#undef RA_WIDE_LAUNCH
+  return ra_check_launch("ra_extend_attention(fused)");
+}
 
 // Argument checks shared with ra_mixed_attention: RA_OK when the call may
 // launch (or has nothing to do), an error status otherwise.
@@ -396,31 +709,11 @@ extern "C" int ra_extend_attention(const void* q, const void* k_new, const void*
                                     max_extend_len, hq, hkv, d, scale, out);
   if (st != RA_OK || batch == 0 || max_extend_len == 0 || total_tokens == 0) return st;
   const int32_t grp = hq / hkv;
-  // Requests with at least 256 query rows per kv head (new tokens x query
-  // heads per kv head) run on the 256-row kernel; shorter ones would leave
-  // most of its tile empty.
-  if (static_cast<int64_t>(max_extend_len) * grp >= kWideMinRows)
-    return ra_extend_wide_launch(q, k_new, v_new, total_tokens, k_pool, v_pool, pool_slots, req_to_token, rtt_rows,
-                                 rtt_stride, req_pool_idx, prefix_lens, extend_lens, extend_start, batch,
-                                 max_extend_len, hq, hkv, d, scale, out, stream);
-  const int32_t tpb = kBM / grp;
-  const int64_t n_qtiles = (static_cast<int64_t>(max_extend_len) + tpb - 1) / tpb;
-  const int64_t items = (static_cast<int64_t>(batch) * hkv * n_qtiles + 7) / 8 * 8;  // whole XCD rounds
-  if (items > INT32_MAX) return ra_fail(RA_EINVAL, "ra_extend_attention: too many work items");
-  const float scale_log2 = scale * RA_LOG2E;
-  auto* qp = static_cast<const __bf16*>(q);
-  auto* knp = static_cast<const __bf16*>(k_new);
-  auto* vnp = static_cast<const __bf16*>(v_new);
-  auto* kp = static_cast<const __bf16*>(k_pool);
-  auto* vp = static_cast<const __bf16*>(v_pool);
-  auto* op = static_cast<__bf16*>(out);
-  const int32_t nq = static_cast<int32_t>(n_qtiles);
-  if (d == 128) {
-    launch<128>(items, stream, qp, knp, vnp, total_tokens, kp, vp, pool_slots, req_to_token, rtt_rows, rtt_stride,
-                req_pool_idx, prefix_lens, extend_lens, extend_start, batch, hkv, grp, nq, scale_log2, op);
-  } else {
-    launch<64>(items, stream, qp, knp, vnp, total_tokens, kp, vp, pool_slots, req_to_token, rtt_rows, rtt_stride,
-               req_pool_idx, prefix_lens, extend_lens, extend_start, batch, hkv, grp, nq, scale_log2, op);
-  }
-  return ra_check_launch("ra_extend_attention");
+  // At least 256 query rows per kv head (new tokens x query heads per kv
+  // head): the 256-row configuration; fewer would leave most of its tile
+  // empty, so they take the 128-row one.
+  const int32_t rows = static_cast<int64_t>(max_extend_len) * grp >= 256 ? 256 : 128;
+  return extend_launch(q, k_new, v_new, total_tokens, k_pool, v_pool, pool_slots, req_to_token, rtt_rows, rtt_stride,
+                       req_pool_idx, prefix_lens, extend_lens, extend_start, batch, max_extend_len, hq, hkv, d,
+                       scale, out, rows, stream);
 }

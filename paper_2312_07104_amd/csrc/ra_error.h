@@ -26,11 +26,3 @@ int ra_decode_validate(const void* q, const void* k_pool, const void* v_pool, in
                        float scale, int32_t num_splits, const void* workspace, size_t workspace_bytes,
                        const void* out);
 
-// Launch of the 256-row extend kernel (extend_wide.hip) for arguments that
-// ra_extend_validate accepted and that hold at least one extend row.
-int ra_extend_wide_launch(const void* q, const void* k_new, const void* v_new, int64_t total_tokens,
-                          const void* k_pool, const void* v_pool, int64_t pool_slots, const int32_t* req_to_token,
-                          int64_t rtt_rows, int64_t rtt_stride, const int32_t* req_pool_idx,
-                          const int32_t* prefix_lens, const int32_t* extend_lens, const int32_t* extend_start,
-                          int32_t batch, int32_t max_extend_len, int32_t hq, int32_t hkv, int32_t d, float scale,
-                          void* out, hipStream_t stream);
