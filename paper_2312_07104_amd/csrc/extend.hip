@@ -456,6 +456,16 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void extend_kernel(
       p[v] = ra_exp2(__builtin_fmaf(sc[bb][j][i], scale_log2, mb[j]));
       if (v & 1) pw[v >> 1] = ra_pack_bf16x2(p[v - 1], p[v]);
     };
+    // The same in three stages, so that the steps of one probability sit in
+    // different MFMA groups and never wait on each other's latency.
+    auto prob_fma = [&](int v) {
+      const int j = v >> 3, bb = (v >> 2) & 1, i = v & 3;
+      p[v] = __builtin_fmaf(sc[bb][j][i], scale_log2, mb[j]);
+    };
+    auto prob_exp = [&](int v) { p[v] = ra_exp2(p[v]); };
+    auto prob_pack = [&](int v) {
+      if (v & 1) pw[v >> 1] = ra_pack_bf16x2(p[v - 1], p[v]);
+    };
     if constexpr (HAS_NEXT) {
 #pragma unroll
       for (int ks = 0; ks < KP; ++ks)
@@ -464,17 +474,30 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void extend_kernel(
       __builtin_amdgcn_sched_barrier(0);
       constexpr int PPG = (NP + NS - 1) / NS;  // probabilities per S^T MFMA
 #pragma unroll
+      for (int v = 0; v < PPG && v < NP; ++v) prob_fma(v);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
       for (int n = 0; n < NS; ++n) {
         const int ks = n / (2 * kQB), bb = (n / kQB) & 1, j = n % kQB;
         if (ks == 0) s_mfma_first(sn[bb][j], kf[ks][bb], qT[j][ks]);
         else s_mfma_acc(sn[bb][j], kf[ks][bb], qT[j][ks]);
+        // group n: fma of the next group's values, exp of this group's,
+        // packs of the previous group's
 #pragma unroll
-        for (int v = n * PPG; v < (n + 1) * PPG && v < NP; ++v) prob(v);
+        for (int v = (n + 1) * PPG; v < (n + 2) * PPG && v < NP; ++v) prob_fma(v);
+#pragma unroll
+        for (int v = n * PPG; v < (n + 1) * PPG && v < NP; ++v) prob_exp(v);
+#pragma unroll
+        for (int v = (n - 1) * PPG; v < n * PPG && v >= 0 && v < NP; ++v) prob_pack(v);
         if (n % (2 * kQB) == 2 * kQB - 1 && ks + 2 < KS) read_k(ks + 2);
         // the first V^T operands, spread over the last S^T MFMAs
         if (n >= NS - VA && n - (NS - VA) < DB) read_v(n - (NS - VA));
         __builtin_amdgcn_sched_barrier(0);
       }
+#pragma unroll
+      for (int v = (NS - 1) * PPG; v < NS * PPG && v < NP; ++v) prob_pack(v);
+#pragma unroll
+      for (int v = NS * PPG; v < NP; ++v) prob(v);
     } else {
 #pragma unroll
       for (int db = 0; db < VA && db < DB; ++db) read_v(db);
