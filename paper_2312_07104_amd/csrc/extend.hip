@@ -559,6 +559,19 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void extend_kernel(
   f32x4_t sa[2][kQB], sb[2][kQB];
   float mt[kQB];
   bf16x8_t kpre[KP][2];
+  // A wave whose 32 query rows are all past the request's last new token
+  // (short extends leave part of the tile empty) still takes every tile
+  // barrier and issues its share of each tile's copies, but computes
+  // nothing, leaving its SIMD to the other wave.
+  if (tok0 + (32 * wave) / grp >= tok_end) {
+    for (int u = 0; u < n_tiles; ++u) {
+      tile_top(u);
+#pragma unroll
+      for (int i = 0; i < 2 * LOADS; ++i) issue_copy(cp, i);
+    }
+    ra_wait_vmcnt<0>();
+    return;
+  }
   tile_top(0);
 #pragma unroll
   for (int i = 0; i < 2 * LOADS; ++i) issue_copy(cp, i);
