@@ -83,3 +83,60 @@ def test_mixed_fits_pool():
     assert all(1024 <= r.prefix_len <= 8192 and 256 <= r.extend_len <= 2048 for r in ph.extend)
     assert all(1024 <= r.seq_len <= 16384 for r in ph.decode)
     assert S.unique_context_tokens(sc) <= 0.9 * sc.pool_slots
+
+
+def test_jump_forward_and_shard_recipes():
+    jf = S.jump_forward()
+    ph = jf.phases[0]
+    assert len(ph.extend) == 256 and (jf.hq, jf.hkv, jf.d) == (32, 8, 128)
+    assert all(1024 <= r.prefix_len <= 8192 and 2 <= r.extend_len <= 32 for r in ph.extend)
+    assert all(len(r.tokens) == r.prefix_len + r.extend_len for r in ph.extend)
+    assert S.unique_context_tokens(jf) <= 0.9 * jf.pool_slots
+    # a head shard keeps every request and token of its base workload
+    for shard, base, heads in (("decode_chat_tp4", S.cfg3_decode_chat, (8, 2)),
+                               ("branching_tp4", S.cfg4_branching, (8, 2))):
+        a, b = S.ALL[shard](), base()
+        assert (a.hq, a.hkv) == heads and a.seed == b.seed and a.pool_slots == b.pool_slots
+        for pa_, pb_ in zip(a.phases, b.phases):
+            for ra, rb in zip(pa_.decode + pa_.extend, pb_.decode + pb_.extend):
+                assert np.array_equal(ra.tokens, rb.tokens)
+
+
+def test_bench_work_accounting_and_bound():
+    """bench.py's algorithmic work: flops over unmasked pairs, per-request
+    and distinct-row bytes, and the roofline bound picked from intensity."""
+    import importlib.util
+    import os
+    import sys
+
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    spec = importlib.util.spec_from_file_location("bench_mod", os.path.join(root, "bench.py"))
+    bench = importlib.util.module_from_spec(spec)
+    argv, sys.argv = sys.argv, ["bench"]
+    try:
+        spec.loader.exec_module(bench)
+    finally:
+        sys.argv = argv
+
+    class Inp:
+        pass
+
+    sc = S.cfg2_extend_fewshot()
+    inp = Inp()
+    inp.ext_meta = [(r.tokens, r.prefix_len, r.extend_len, 0) for r in sc.phases[0].extend]
+    inp.dec_meta, inp.n_dec = [], 0
+    w = bench.algorithmic_work(sc, inp)
+    # 64 requests x 32 heads x 4 D flops per unmasked (query, key) pair
+    assert w["pairs"] == 64 * (128 * 2048 + 128 * 129 // 2)
+    assert w["ext_flops"] == 4.0 * 128 * 32 * w["pairs"]
+    # distinct rows: the shared 2048-token prefix once, each request's 128 new tokens
+    row = 2 * 32 * 128 * 2
+    assert w["ext_unique_bytes"] == (2048 + 64 * 128) * row + 64 * 128 * 2 * 32 * 128 * 2
+    ridge = bench.BF16_PEAK_TFLOPS * 1e12 / (bench.HBM_PEAK_GBS * 1e9)
+    assert w["ext_flops"] / w["ext_unique_bytes"] > ridge      # few-shot extend: MFMA-bound
+    jf = S.jump_forward(n_req=16)
+    inp2 = Inp()
+    inp2.ext_meta = [(r.tokens, r.prefix_len, r.extend_len, 0) for r in jf.phases[0].extend]
+    inp2.dec_meta, inp2.n_dec = [], 0
+    w2 = bench.algorithmic_work(jf, inp2)
+    assert w2["ext_flops"] / w2["ext_unique_bytes"] < ridge    # short extends: HBM-bound
