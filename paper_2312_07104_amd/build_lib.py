@@ -56,7 +56,9 @@ def build(verbose: bool = False) -> str:
         if src.endswith(".hip"):
             cmds.append([HIPCC, *COMMON, *HIP_ONLY, *EXTRA.get(os.path.basename(src), []), "-c", src, "-o", obj])
         else:
-            cmds.append([HIPCC, *COMMON, "-c", src, "-o", obj])
+            # Host sources still go through hipcc for the HIP runtime headers;
+            # name the target so no default-architecture code object is made.
+            cmds.append([HIPCC, *COMMON, f"--offload-arch={ARCH}", "-c", src, "-o", obj])
     with cf.ThreadPoolExecutor(max_workers=min(8, os.cpu_count() or 1)) as ex:
         for r in ex.map(_run, cmds):
             if verbose and (r.stdout or r.stderr):

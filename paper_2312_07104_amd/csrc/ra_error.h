@@ -3,6 +3,7 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include <new>
 #include <string>
 
 #include <hip/hip_runtime.h>
@@ -11,6 +12,29 @@
 
 int ra_fail(int code, const std::string& msg);
 int ra_ok();
+
+// Runs a host entry point's body so that no C++ exception crosses the C ABI:
+// running out of host memory becomes RA_ENOMEM, anything else RA_EINVAL.  A
+// tree or router whose operation failed this way may be left part-way through
+// the operation; the caller should destroy it.
+template <class F>
+int ra_guard(const char* who, F&& body) noexcept {
+  try {
+    return body();
+  } catch (const std::bad_alloc&) {
+    try {
+      return ra_fail(RA_ENOMEM, std::string(who) + ": out of host memory");
+    } catch (...) {
+      return RA_ENOMEM;
+    }
+  } catch (...) {
+    try {
+      return ra_fail(RA_EINVAL, std::string(who) + ": internal error");
+    } catch (...) {
+      return RA_EINVAL;
+    }
+  }
+}
 
 // Argument checks of the attention entry points (no launch), shared with the
 // mixed-batch call so that it can reject a bad batch before queuing anything.

@@ -21,6 +21,7 @@
 #include <cstdint>
 #include <cstring>
 #include <deque>
+#include <memory>
 #include <set>
 #include <string>
 #include <unordered_map>
@@ -171,42 +172,44 @@ struct ra_cache {
 extern "C" {
 
 int ra_cache_create(int64_t pool_slots, const int32_t* order, ra_cache** out) {
-  if (!out) return ra_fail(RA_EINVAL, "ra_cache_create: out is NULL");
-  if (pool_slots < 0 || pool_slots > INT32_MAX)
-    return ra_fail(RA_EINVAL, "ra_cache_create: pool_slots out of range");
-  ra_cache* c = new ra_cache();
-  c->pool_slots = pool_slots;
-  c->ring.resize(static_cast<size_t>(pool_slots));
-  c->is_free.assign(static_cast<size_t>(pool_slots), 0);
-  for (int64_t i = 0; i < pool_slots; ++i) {
-    int32_t s = order ? order[i] : static_cast<int32_t>(i);
-    if (s < 0 || s >= pool_slots || c->is_free[s]) {
-      delete c;
-      return ra_fail(RA_EINVAL, "ra_cache_create: initial order is not a permutation");
+  return ra_guard("ra_cache_create", [&]() -> int {
+    if (!out) return ra_fail(RA_EINVAL, "ra_cache_create: out is NULL");
+    if (pool_slots < 0 || pool_slots > INT32_MAX)
+      return ra_fail(RA_EINVAL, "ra_cache_create: pool_slots out of range");
+    std::unique_ptr<ra_cache> c(new ra_cache());
+    c->pool_slots = pool_slots;
+    c->ring.resize(static_cast<size_t>(pool_slots));
+    c->is_free.assign(static_cast<size_t>(pool_slots), 0);
+    for (int64_t i = 0; i < pool_slots; ++i) {
+      int32_t s = order ? order[i] : static_cast<int32_t>(i);
+      if (s < 0 || s >= pool_slots || c->is_free[s])
+        return ra_fail(RA_EINVAL, "ra_cache_create: initial order is not a permutation");
+      c->push_free(s);
     }
-    c->push_free(s);
-  }
-  c->nodes.emplace_back();  // root
-  c->nodes[0].alive = true;
-  *out = c;
-  return ra_ok();
+    c->nodes.emplace_back();  // root
+    c->nodes[0].alive = true;
+    *out = c.release();
+    return ra_ok();
+  });
 }
 
 void ra_cache_destroy(ra_cache* c) { delete c; }
 
 int ra_match_prefix(ra_cache* c, const int32_t* tokens, int64_t n, int32_t* out_slots,
                     int64_t* out_len, int64_t* out_node) {
-  if (!c || n < 0 || (n > 0 && !tokens)) return ra_fail(RA_EINVAL, "ra_match_prefix: bad argument");
-  int64_t pos = 0;
-  int64_t node = c->walk(tokens, n, &pos, [&](int64_t ch, int64_t p) {
-    if (out_slots) {
-      const auto& s = c->nodes[ch].slots;
-      std::memcpy(out_slots + p, s.data(), s.size() * sizeof(int32_t));
-    }
+  return ra_guard("ra_match_prefix", [&]() -> int {
+    if (!c || n < 0 || (n > 0 && !tokens)) return ra_fail(RA_EINVAL, "ra_match_prefix: bad argument");
+    int64_t pos = 0;
+    int64_t node = c->walk(tokens, n, &pos, [&](int64_t ch, int64_t p) {
+      if (out_slots) {
+        const auto& s = c->nodes[ch].slots;
+        std::memcpy(out_slots + p, s.data(), s.size() * sizeof(int32_t));
+      }
+    });
+    if (out_len) *out_len = pos;
+    if (out_node) *out_node = node;
+    return ra_ok();
   });
-  if (out_len) *out_len = pos;
-  if (out_node) *out_node = node;
-  return ra_ok();
 }
 
 static bool valid_node(const ra_cache* c, int64_t node) {
@@ -214,41 +217,47 @@ static bool valid_node(const ra_cache* c, int64_t node) {
 }
 
 int ra_inc_ref(ra_cache* c, int64_t node, int64_t* out_delta) {
-  if (!c || !valid_node(c, node)) return ra_fail(RA_EINVAL, "ra_inc_ref: unknown node");
-  int64_t delta = 0;
-  for (int64_t x = node; x != 0; x = c->nodes[x].parent) {
-    Node& n = c->nodes[x];
-    if (n.ref == 0) {
-      delta -= static_cast<int64_t>(n.key.size());
+  return ra_guard("ra_inc_ref", [&]() -> int {
+    if (!c || !valid_node(c, node)) return ra_fail(RA_EINVAL, "ra_inc_ref: unknown node");
+    int64_t delta = 0;
+    for (int64_t x = node; x != 0; x = c->nodes[x].parent) {
+      Node& n = c->nodes[x];
+      if (n.ref == 0) {
+        delta -= static_cast<int64_t>(n.key.size());
+      }
+      ++n.ref;
+      c->refresh(x);
     }
-    ++n.ref;
-    c->refresh(x);
-  }
-  c->evictable += delta;
-  if (out_delta) *out_delta = delta;
-  return ra_ok();
+    c->evictable += delta;
+    if (out_delta) *out_delta = delta;
+    return ra_ok();
+  });
 }
 
 int ra_dec_ref(ra_cache* c, int64_t node, int64_t* out_delta) {
-  if (!c || !valid_node(c, node)) return ra_fail(RA_EINVAL, "ra_dec_ref: unknown node");
-  for (int64_t x = node; x != 0; x = c->nodes[x].parent)
-    if (c->nodes[x].ref == 0) return ra_fail(RA_EINVAL, "ra_dec_ref: reference counter underflow");
-  int64_t delta = 0;
-  for (int64_t x = node; x != 0; x = c->nodes[x].parent) {
-    Node& n = c->nodes[x];
-    if (--n.ref == 0) delta += static_cast<int64_t>(n.key.size());
-    c->refresh(x);
-  }
-  c->evictable += delta;
-  if (out_delta) *out_delta = delta;
-  return ra_ok();
+  return ra_guard("ra_dec_ref", [&]() -> int {
+    if (!c || !valid_node(c, node)) return ra_fail(RA_EINVAL, "ra_dec_ref: unknown node");
+    for (int64_t x = node; x != 0; x = c->nodes[x].parent)
+      if (c->nodes[x].ref == 0) return ra_fail(RA_EINVAL, "ra_dec_ref: reference counter underflow");
+    int64_t delta = 0;
+    for (int64_t x = node; x != 0; x = c->nodes[x].parent) {
+      Node& n = c->nodes[x];
+      if (--n.ref == 0) delta += static_cast<int64_t>(n.key.size());
+      c->refresh(x);
+    }
+    c->evictable += delta;
+    if (out_delta) *out_delta = delta;
+    return ra_ok();
+  });
 }
 
 int ra_alloc_slots(ra_cache* c, int64_t n, int32_t* out_slots) {
-  if (!c || n < 0 || (n > 0 && !out_slots)) return ra_fail(RA_EINVAL, "ra_alloc_slots: bad argument");
-  if (n > c->count) return ra_fail(RA_ENOMEM, "ra_alloc_slots: not enough free slots");
-  for (int64_t i = 0; i < n; ++i) out_slots[i] = c->pop_free();
-  return ra_ok();
+  return ra_guard("ra_alloc_slots", [&]() -> int {
+    if (!c || n < 0 || (n > 0 && !out_slots)) return ra_fail(RA_EINVAL, "ra_alloc_slots: bad argument");
+    if (n > c->count) return ra_fail(RA_ENOMEM, "ra_alloc_slots: not enough free slots");
+    for (int64_t i = 0; i < n; ++i) out_slots[i] = c->pop_free();
+    return ra_ok();
+  });
 }
 
 static int check_freeable(ra_cache* c, const int32_t* slots, int64_t n, const char* who) {
@@ -267,103 +276,109 @@ static int check_freeable(ra_cache* c, const int32_t* slots, int64_t n, const ch
 }
 
 int ra_free_slots(ra_cache* c, const int32_t* slots, int64_t n) {
-  if (!c || n < 0 || (n > 0 && !slots)) return ra_fail(RA_EINVAL, "ra_free_slots: bad argument");
-  int st = check_freeable(c, slots, n, "ra_free_slots");
-  if (st != RA_OK) return st;
-  for (int64_t i = 0; i < n; ++i) c->push_free(slots[i]);
-  return ra_ok();
+  return ra_guard("ra_free_slots", [&]() -> int {
+    if (!c || n < 0 || (n > 0 && !slots)) return ra_fail(RA_EINVAL, "ra_free_slots: bad argument");
+    int st = check_freeable(c, slots, n, "ra_free_slots");
+    if (st != RA_OK) return st;
+    for (int64_t i = 0; i < n; ++i) c->push_free(slots[i]);
+    return ra_ok();
+  });
 }
 
 int ra_insert(ra_cache* c, const int32_t* tokens, const int32_t* slots, int64_t n,
               int64_t* out_cached, int64_t* out_node) {
-  if (!c || n < 0 || (n > 0 && (!tokens || !slots))) return ra_fail(RA_EINVAL, "ra_insert: bad argument");
-  // Validate duplicates before changing anything: walk read-only first.
-  {
-    int64_t node = 0, pos = 0;
-    std::vector<int32_t> dup;
-    while (pos < n) {
-      auto it = c->children.find(edge_key(node, tokens[pos]));
-      if (it == c->children.end()) break;
-      const Node& ch = c->nodes[it->second];
-      int64_t lim = std::min<int64_t>(static_cast<int64_t>(ch.key.size()), n - pos);
-      int64_t k = 0;
-      while (k < lim && ch.key[k] == tokens[pos + k]) {
-        if (slots[pos + k] != ch.slots[k]) dup.push_back(slots[pos + k]);
-        ++k;
+  return ra_guard("ra_insert", [&]() -> int {
+    if (!c || n < 0 || (n > 0 && (!tokens || !slots))) return ra_fail(RA_EINVAL, "ra_insert: bad argument");
+    // Validate duplicates before changing anything: walk read-only first.
+    {
+      int64_t node = 0, pos = 0;
+      std::vector<int32_t> dup;
+      while (pos < n) {
+        auto it = c->children.find(edge_key(node, tokens[pos]));
+        if (it == c->children.end()) break;
+        const Node& ch = c->nodes[it->second];
+        int64_t lim = std::min<int64_t>(static_cast<int64_t>(ch.key.size()), n - pos);
+        int64_t k = 0;
+        while (k < lim && ch.key[k] == tokens[pos + k]) {
+          if (slots[pos + k] != ch.slots[k]) dup.push_back(slots[pos + k]);
+          ++k;
+        }
+        pos += k;
+        if (k < static_cast<int64_t>(ch.key.size())) break;
+        node = it->second;
       }
-      pos += k;
-      if (k < static_cast<int64_t>(ch.key.size())) break;
-      node = it->second;
+      if (!dup.empty()) {
+        int st = check_freeable(c, dup.data(), static_cast<int64_t>(dup.size()), "ra_insert");
+        if (st != RA_OK) return st;
+      }
+      // slots that will enter the tree must be allocated pool slots
+      for (int64_t i = pos; i < n; ++i)
+        if (slots[i] < 0 || slots[i] >= c->pool_slots || c->is_free[slots[i]])
+          return ra_fail(RA_EINVAL, "ra_insert: new slot out of range or free");
     }
-    if (!dup.empty()) {
-      int st = check_freeable(c, dup.data(), static_cast<int64_t>(dup.size()), "ra_insert");
-      if (st != RA_OK) return st;
+    std::vector<int32_t> dup;
+    int64_t pos = 0;
+    int64_t node = c->walk(tokens, n, &pos, [&](int64_t ch, int64_t p) {
+      const auto& s = c->nodes[ch].slots;
+      for (size_t i = 0; i < s.size(); ++i)
+        if (slots[p + i] != s[i]) dup.push_back(slots[p + i]);
+    });
+    for (int32_t s : dup) c->push_free(s);
+    int64_t cached = pos;
+    if (pos < n) {
+      int64_t leaf = c->new_node(node, std::vector<int32_t>(tokens + pos, tokens + n),
+                                 std::vector<int32_t>(slots + pos, slots + n), 0, c->clock);
+      c->children[edge_key(node, tokens[pos])] = leaf;
+      c->nodes[node].n_children += 1;
+      c->evictable += n - pos;
+      c->cached += n - pos;
+      c->refresh(node);
+      c->refresh(leaf);
+      node = leaf;
     }
-    // slots that will enter the tree must be allocated pool slots
-    for (int64_t i = pos; i < n; ++i)
-      if (slots[i] < 0 || slots[i] >= c->pool_slots || c->is_free[slots[i]])
-        return ra_fail(RA_EINVAL, "ra_insert: new slot out of range or free");
-  }
-  std::vector<int32_t> dup;
-  int64_t pos = 0;
-  int64_t node = c->walk(tokens, n, &pos, [&](int64_t ch, int64_t p) {
-    const auto& s = c->nodes[ch].slots;
-    for (size_t i = 0; i < s.size(); ++i)
-      if (slots[p + i] != s[i]) dup.push_back(slots[p + i]);
+    if (out_cached) *out_cached = cached;
+    if (out_node) *out_node = node;
+    return ra_ok();
   });
-  for (int32_t s : dup) c->push_free(s);
-  int64_t cached = pos;
-  if (pos < n) {
-    int64_t leaf = c->new_node(node, std::vector<int32_t>(tokens + pos, tokens + n),
-                               std::vector<int32_t>(slots + pos, slots + n), 0, c->clock);
-    c->children[edge_key(node, tokens[pos])] = leaf;
-    c->nodes[node].n_children += 1;
-    c->evictable += n - pos;
-    c->cached += n - pos;
-    c->refresh(node);
-    c->refresh(leaf);
-    node = leaf;
-  }
-  if (out_cached) *out_cached = cached;
-  if (out_node) *out_node = node;
-  return ra_ok();
 }
 
 int ra_evict(ra_cache* c, int64_t n_tokens, int64_t* out_freed) {
-  if (!c) return ra_fail(RA_EINVAL, "ra_evict: cache is NULL");
-  int64_t freed = 0;
-  while (freed < n_tokens && !c->lru.empty()) {
-    int64_t x = c->lru.begin()->second;
-    c->lru.erase(c->lru.begin());
-    Node& n = c->nodes[x];
-    n.in_lru = false;
-    if (c->log_evictions) {
-      ra_cache::Evicted e;
-      e.len = static_cast<int64_t>(n.key.size());
-      std::vector<int64_t> chain;
-      for (int64_t y = x; y != 0; y = c->nodes[y].parent) chain.push_back(y);
-      for (auto it = chain.rbegin(); it != chain.rend(); ++it) {
-        const auto& k = c->nodes[*it].key;
-        e.path.insert(e.path.end(), k.begin(), k.end());
+  return ra_guard("ra_evict", [&]() -> int {
+    if (!c) return ra_fail(RA_EINVAL, "ra_evict: cache is NULL");
+    int64_t freed = 0;
+    while (freed < n_tokens && !c->lru.empty()) {
+      int64_t x = c->lru.begin()->second;
+      c->lru.erase(c->lru.begin());
+      Node& n = c->nodes[x];
+      n.in_lru = false;
+      if (c->log_evictions) {
+        ra_cache::Evicted e;
+        e.len = static_cast<int64_t>(n.key.size());
+        std::vector<int64_t> chain;
+        for (int64_t y = x; y != 0; y = c->nodes[y].parent) chain.push_back(y);
+        for (auto it = chain.rbegin(); it != chain.rend(); ++it) {
+          const auto& k = c->nodes[*it].key;
+          e.path.insert(e.path.end(), k.begin(), k.end());
+        }
+        c->eviction_log.push_back(std::move(e));
       }
-      c->eviction_log.push_back(std::move(e));
+      for (int32_t s : n.slots) c->push_free(s);
+      int64_t len = static_cast<int64_t>(n.key.size());
+      freed += len;
+      c->evictable -= len;
+      c->cached -= len;
+      c->children.erase(edge_key(n.parent, n.key[0]));
+      int64_t par = n.parent;
+      n.alive = false;
+      std::vector<int32_t>().swap(n.key);
+      std::vector<int32_t>().swap(n.slots);
+      --c->live;
+      c->nodes[par].n_children -= 1;
+      c->refresh(par);
     }
-    for (int32_t s : n.slots) c->push_free(s);
-    int64_t len = static_cast<int64_t>(n.key.size());
-    freed += len;
-    c->evictable -= len;
-    c->cached -= len;
-    c->children.erase(edge_key(n.parent, n.key[0]));
-    int64_t par = n.parent;
-    n.alive = false;
-    std::vector<int32_t>().swap(n.key);
-    std::vector<int32_t>().swap(n.slots);
-    --c->live;
-    c->nodes[par].n_children -= 1;
-    c->refresh(par);
-  }
-  if (out_freed) *out_freed = freed;
-  return ra_ok();
+    if (out_freed) *out_freed = freed;
+    return ra_ok();
+  });
 }
 
 int ra_cache_log_evictions(ra_cache* c, int32_t enable) {
@@ -374,20 +389,22 @@ int ra_cache_log_evictions(ra_cache* c, int32_t enable) {
 }
 
 int ra_eviction_log_pop(ra_cache* c, int32_t* tokens, int64_t cap, int64_t* out_path_len, int64_t* out_evicted_len) {
-  if (!c || !out_path_len) return ra_fail(RA_EINVAL, "ra_eviction_log_pop: NULL argument");
-  if (c->eviction_log.empty()) {
-    *out_path_len = -1;
-    if (out_evicted_len) *out_evicted_len = 0;
+  return ra_guard("ra_eviction_log_pop", [&]() -> int {
+    if (!c || !out_path_len) return ra_fail(RA_EINVAL, "ra_eviction_log_pop: NULL argument");
+    if (c->eviction_log.empty()) {
+      *out_path_len = -1;
+      if (out_evicted_len) *out_evicted_len = 0;
+      return ra_ok();
+    }
+    const auto& e = c->eviction_log.front();
+    const int64_t n = static_cast<int64_t>(e.path.size());
+    *out_path_len = n;
+    if (out_evicted_len) *out_evicted_len = e.len;
+    if (!tokens || cap < n) return ra_fail(RA_EINVAL, "ra_eviction_log_pop: token buffer too small");
+    std::memcpy(tokens, e.path.data(), sizeof(int32_t) * n);
+    c->eviction_log.pop_front();
     return ra_ok();
-  }
-  const auto& e = c->eviction_log.front();
-  const int64_t n = static_cast<int64_t>(e.path.size());
-  *out_path_len = n;
-  if (out_evicted_len) *out_evicted_len = e.len;
-  if (!tokens || cap < n) return ra_fail(RA_EINVAL, "ra_eviction_log_pop: token buffer too small");
-  std::memcpy(tokens, e.path.data(), sizeof(int32_t) * n);
-  c->eviction_log.pop_front();
-  return ra_ok();
+  });
 }
 
 int64_t ra_evictable_size(const ra_cache* c) { return c ? c->evictable : 0; }
@@ -396,30 +413,32 @@ int64_t ra_cached_tokens(const ra_cache* c) { return c ? c->cached : 0; }
 int64_t ra_num_nodes(const ra_cache* c) { return c ? c->live : 0; }
 
 int ra_snapshot(const ra_cache* c, int64_t* buf, int64_t cap, int64_t* out_len) {
-  if (!c) return ra_fail(RA_EINVAL, "ra_snapshot: cache is NULL");
-  int64_t need = 3 + c->count;
-  for (const Node& n : c->nodes)
-    if (n.alive) need += 5 + 2 * static_cast<int64_t>(n.key.size());
-  if (out_len) *out_len = need;
-  if (!buf) return ra_ok();
-  if (cap < need) return ra_fail(RA_EINVAL, "ra_snapshot: buffer too small");
-  int64_t* w = buf;
-  *w++ = static_cast<int64_t>(c->clock);
-  *w++ = c->live;
-  *w++ = c->count;
-  for (size_t id = 0; id < c->nodes.size(); ++id) {
-    const Node& n = c->nodes[id];
-    if (!n.alive) continue;
-    *w++ = static_cast<int64_t>(id);
-    *w++ = n.parent;
-    *w++ = n.ref;
-    *w++ = static_cast<int64_t>(n.stamp);
-    *w++ = static_cast<int64_t>(n.key.size());
-    for (int32_t t : n.key) *w++ = t;
-    for (int32_t s : n.slots) *w++ = s;
-  }
-  for (int64_t i = 0; i < c->count; ++i) *w++ = c->ring[(c->head + i) % c->pool_slots];
-  return ra_ok();
+  return ra_guard("ra_snapshot", [&]() -> int {
+    if (!c) return ra_fail(RA_EINVAL, "ra_snapshot: cache is NULL");
+    int64_t need = 3 + c->count;
+    for (const Node& n : c->nodes)
+      if (n.alive) need += 5 + 2 * static_cast<int64_t>(n.key.size());
+    if (out_len) *out_len = need;
+    if (!buf) return ra_ok();
+    if (cap < need) return ra_fail(RA_EINVAL, "ra_snapshot: buffer too small");
+    int64_t* w = buf;
+    *w++ = static_cast<int64_t>(c->clock);
+    *w++ = c->live;
+    *w++ = c->count;
+    for (size_t id = 0; id < c->nodes.size(); ++id) {
+      const Node& n = c->nodes[id];
+      if (!n.alive) continue;
+      *w++ = static_cast<int64_t>(id);
+      *w++ = n.parent;
+      *w++ = n.ref;
+      *w++ = static_cast<int64_t>(n.stamp);
+      *w++ = static_cast<int64_t>(n.key.size());
+      for (int32_t t : n.key) *w++ = t;
+      for (int32_t s : n.slots) *w++ = s;
+    }
+    for (int64_t i = 0; i < c->count; ++i) *w++ = c->ring[(c->head + i) % c->pool_slots];
+    return ra_ok();
+  });
 }
 
 }  // extern "C"

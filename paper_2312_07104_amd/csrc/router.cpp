@@ -13,6 +13,7 @@
 // becomes empty and that has no children is removed, and so is its parent
 // when that leaves it empty and childless.
 #include <cstdint>
+#include <memory>
 #include <string>
 #include <unordered_map>
 #include <vector>
@@ -125,109 +126,116 @@ struct ra_router {
 extern "C" {
 
 int ra_router_create(int32_t n_workers, ra_router** out) {
-  if (!out) return ra_fail(RA_EINVAL, "ra_router_create: out is NULL");
-  *out = nullptr;
-  if (n_workers < 1 || n_workers > 64) return ra_fail(RA_EINVAL, "ra_router_create: n_workers must be in [1, 64]");
-  auto* r = new (std::nothrow) ra_router;
-  if (!r) return ra_fail(RA_ENOMEM, "ra_router_create: out of host memory");
-  r->n_workers = n_workers;
-  r->nodes.emplace_back();
-  r->nodes[0].alive = true;
-  r->nodes[0].mask = n_workers == 64 ? ~0ull : ((1ull << n_workers) - 1);  // every worker holds the empty prefix
-  r->held.assign(n_workers, 0);
-  *out = r;
-  return ra_ok();
+  return ra_guard("ra_router_create", [&]() -> int {
+    if (!out) return ra_fail(RA_EINVAL, "ra_router_create: out is NULL");
+    *out = nullptr;
+    if (n_workers < 1 || n_workers > 64) return ra_fail(RA_EINVAL, "ra_router_create: n_workers must be in [1, 64]");
+    std::unique_ptr<ra_router> r(new ra_router);
+    r->n_workers = n_workers;
+    r->nodes.emplace_back();
+    r->nodes[0].alive = true;
+    r->nodes[0].mask = n_workers == 64 ? ~0ull : ((1ull << n_workers) - 1);  // every worker holds the empty prefix
+    r->held.assign(n_workers, 0);
+    *out = r.release();
+    return ra_ok();
+  });
 }
 
 void ra_router_destroy(ra_router* r) { delete r; }
 
 int ra_router_match(const ra_router* r, const int32_t* tokens, int64_t n, int64_t* out_len) {
-  if (!r || !out_len || (n > 0 && !tokens) || n < 0) return ra_fail(RA_EINVAL, "ra_router_match: bad argument");
-  for (int32_t w = 0; w < r->n_workers; ++w) out_len[w] = 0;
-  int64_t node = 0, pos = 0;
-  while (pos < n) {
-    auto it = r->children.find(edge(node, tokens[pos]));
-    if (it == r->children.end()) break;
-    const MNode& x = r->nodes[it->second];
-    int64_t j = 0;
-    const int64_t kl = static_cast<int64_t>(x.key.size());
-    while (j < kl && pos + j < n && x.key[j] == tokens[pos + j]) ++j;
-    pos += j;
-    for (uint64_t m = x.mask; m; m &= m - 1) out_len[__builtin_ctzll(m)] = pos;
-    if (j < kl || x.mask == 0) break;
-    node = it->second;
-  }
-  return ra_ok();
+  return ra_guard("ra_router_match", [&]() -> int {
+    if (!r || !out_len || (n > 0 && !tokens) || n < 0) return ra_fail(RA_EINVAL, "ra_router_match: bad argument");
+    for (int32_t w = 0; w < r->n_workers; ++w) out_len[w] = 0;
+    int64_t node = 0, pos = 0;
+    while (pos < n) {
+      auto it = r->children.find(edge(node, tokens[pos]));
+      if (it == r->children.end()) break;
+      const MNode& x = r->nodes[it->second];
+      int64_t j = 0;
+      const int64_t kl = static_cast<int64_t>(x.key.size());
+      while (j < kl && pos + j < n && x.key[j] == tokens[pos + j]) ++j;
+      pos += j;
+      for (uint64_t m = x.mask; m; m &= m - 1) out_len[__builtin_ctzll(m)] = pos;
+      if (j < kl || x.mask == 0) break;
+      node = it->second;
+    }
+    return ra_ok();
+  });
 }
 
 int ra_router_insert(ra_router* r, int32_t worker, const int32_t* tokens, int64_t n) {
-  if (!r || worker < 0 || worker >= r->n_workers || n < 0 || (n > 0 && !tokens))
-    return ra_fail(RA_EINVAL, "ra_router_insert: bad argument");
-  const uint64_t b = 1ull << worker;
-  int64_t node = 0, pos = 0;
-  while (pos < n) {
-    auto it = r->children.find(edge(node, tokens[pos]));
-    if (it == r->children.end()) {
-      const int64_t leaf = r->new_node();
-      MNode& L = r->nodes[leaf];
-      L.parent = node;
-      L.key.assign(tokens + pos, tokens + n);
-      L.mask = b;
-      r->children[edge(node, tokens[pos])] = leaf;
-      r->nodes[node].kids.push_back(leaf);
-      r->held[worker] += n - pos;
-      return ra_ok();
+  return ra_guard("ra_router_insert", [&]() -> int {
+    if (!r || worker < 0 || worker >= r->n_workers || n < 0 || (n > 0 && !tokens))
+      return ra_fail(RA_EINVAL, "ra_router_insert: bad argument");
+    const uint64_t b = 1ull << worker;
+    int64_t node = 0, pos = 0;
+    while (pos < n) {
+      auto it = r->children.find(edge(node, tokens[pos]));
+      if (it == r->children.end()) {
+        const int64_t leaf = r->new_node();
+        MNode& L = r->nodes[leaf];
+        L.parent = node;
+        L.key.assign(tokens + pos, tokens + n);
+        L.mask = b;
+        r->children[edge(node, tokens[pos])] = leaf;
+        r->nodes[node].kids.push_back(leaf);
+        r->held[worker] += n - pos;
+        return ra_ok();
+      }
+      int64_t x = it->second;
+      int64_t j = 0;
+      const int64_t kl = static_cast<int64_t>(r->nodes[x].key.size());
+      while (j < kl && pos + j < n && r->nodes[x].key[j] == tokens[pos + j]) ++j;
+      if (j < kl) x = r->split(x, j);
+      MNode& X = r->nodes[x];
+      if (!(X.mask & b)) {
+        X.mask |= b;
+        r->held[worker] += static_cast<int64_t>(X.key.size());
+      }
+      pos += j;
+      node = x;
     }
-    int64_t x = it->second;
-    int64_t j = 0;
-    const int64_t kl = static_cast<int64_t>(r->nodes[x].key.size());
-    while (j < kl && pos + j < n && r->nodes[x].key[j] == tokens[pos + j]) ++j;
-    if (j < kl) x = r->split(x, j);
-    MNode& X = r->nodes[x];
-    if (!(X.mask & b)) {
-      X.mask |= b;
-      r->held[worker] += static_cast<int64_t>(X.key.size());
-    }
-    pos += j;
-    node = x;
-  }
-  return ra_ok();
+    return ra_ok();
+  });
 }
 
 int ra_router_evict(ra_router* r, int32_t worker, const int32_t* tokens, int64_t path_len, int64_t evicted_len) {
-  if (!r || worker < 0 || worker >= r->n_workers || path_len < 0 || evicted_len < 0 || evicted_len > path_len ||
-      (path_len > 0 && !tokens))
-    return ra_fail(RA_EINVAL, "ra_router_evict: bad argument");
-  if (evicted_len == 0) return ra_ok();
-  const uint64_t b = 1ull << worker;
-  const int64_t start = path_len - evicted_len;
-  // Walk the path to position `start`, splitting the node that straddles it,
-  // so that the evicted range begins on a node boundary.
-  int64_t node = 0, pos = 0;
-  while (pos < start) {
-    auto it = r->children.find(edge(node, tokens[pos]));
-    if (it == r->children.end()) return ra_ok();  // the router never saw this range
-    const int64_t x = it->second;
-    const int64_t kl = static_cast<int64_t>(r->nodes[x].key.size());
-    int64_t j = 0;
-    while (j < kl && pos + j < start && r->nodes[x].key[j] == tokens[pos + j]) ++j;
-    if (pos + kl <= start) {
-      if (j < kl) return ra_ok();
-      pos += kl;
-      node = x;
-      continue;
+  return ra_guard("ra_router_evict", [&]() -> int {
+    if (!r || worker < 0 || worker >= r->n_workers || path_len < 0 || evicted_len < 0 || evicted_len > path_len ||
+        (path_len > 0 && !tokens))
+      return ra_fail(RA_EINVAL, "ra_router_evict: bad argument");
+    if (evicted_len == 0) return ra_ok();
+    const uint64_t b = 1ull << worker;
+    const int64_t start = path_len - evicted_len;
+    // Walk the path to position `start`, splitting the node that straddles it,
+    // so that the evicted range begins on a node boundary.
+    int64_t node = 0, pos = 0;
+    while (pos < start) {
+      auto it = r->children.find(edge(node, tokens[pos]));
+      if (it == r->children.end()) return ra_ok();  // the router never saw this range
+      const int64_t x = it->second;
+      const int64_t kl = static_cast<int64_t>(r->nodes[x].key.size());
+      int64_t j = 0;
+      while (j < kl && pos + j < start && r->nodes[x].key[j] == tokens[pos + j]) ++j;
+      if (pos + kl <= start) {
+        if (j < kl) return ra_ok();
+        pos += kl;
+        node = x;
+        continue;
+      }
+      if (j < start - pos) return ra_ok();  // the path leaves the tree before the evicted range
+      node = r->split(x, start - pos);      // the upper part ends at `start`
+      pos = start;
     }
-    if (j < start - pos) return ra_ok();  // the path leaves the tree before the evicted range
-    node = r->split(x, start - pos);      // the upper part ends at `start`
-    pos = start;
-  }
-  // The node that continues the path at `start` heads the evicted range; the
-  // worker held nothing below the evicted leaf, so its bit goes from that
-  // node's whole subtree.
-  auto it = r->children.find(edge(node, tokens[start]));
-  if (it == r->children.end()) return ra_ok();
-  r->clear_subtree(it->second, b, worker);
-  return ra_ok();
+    // The node that continues the path at `start` heads the evicted range; the
+    // worker held nothing below the evicted leaf, so its bit goes from that
+    // node's whole subtree.
+    auto it = r->children.find(edge(node, tokens[start]));
+    if (it == r->children.end()) return ra_ok();
+    r->clear_subtree(it->second, b, worker);
+    return ra_ok();
+  });
 }
 
 int64_t ra_router_num_nodes(const ra_router* r) { return r ? r->live : 0; }
