@@ -176,11 +176,17 @@ def test_branching_two_phases():
 
 
 def test_mixed_full_size_sampled():
+    """The headline batch through the one mixed call (extend and decode on
+    two streams): both outputs equal separate calls bit for bit, and sampled
+    rows match the oracle."""
     sc = S.cfg5_mixed()
     log(f"case: mixed seed={sc.seed} (history replay on host)")
     run = ScenarioRun(sc)
     log(f"history ops={run.history_ops} in {run.history_seconds:.2f}s")
-    inp, oe, od = run_phase(run, 0)
+    inp, oe_sep, od_sep = run_phase(run, 0)
+    oe, od = run.mixed(inp)
+    torch.cuda.synchronize()
+    assert torch.equal(oe, oe_sep) and torch.equal(od, od_sep)
     er = check_extend(run, inp, oe, sample=[0, 13, 31], rows_per_req=16, what="mixed/extend")
     log("mixed extend worst", er)
     lens = np.array([l for _, l in inp.dec_meta])
@@ -228,6 +234,9 @@ def test_tp8_mixed_shard_sampled():
     log(f"case: mixed_tp8 seed={sc.seed} Hq={sc.hq} Hkv={sc.hkv}")
     run = ScenarioRun(sc)
     inp, oe, od = run_phase(run, 0)
+    me, md = run.mixed(inp)  # one kv head, G = 8
+    torch.cuda.synchronize()
+    assert torch.equal(me, oe) and torch.equal(md, od)
     check_extend(run, inp, oe, sample=[1, 30], rows_per_req=12, what="mixed_tp8/extend")
     lens = np.array([l for _, l in inp.dec_meta])
     check_decode(run, inp, od, sample=sorted({int(lens.argmax()), int(lens.argmin()), 77}), what="mixed_tp8/decode")

@@ -264,6 +264,50 @@ def test_mixed_call_equals_separate_calls():
         assert torch.isfinite(s_e) and torch.isfinite(s_d)
 
 
+def test_mixed_call_decode_heavy_equals_separate_calls():
+    """One short extend request beside the whole decode batch (the decode
+    finishes long after the extend): both outputs equal separate calls bit for
+    bit, over repeated calls on one workspace."""
+    sc = S.cfg5_mixed_small()
+    log(f"case: decode-heavy mixed call seed={sc.seed}")
+    run = ScenarioRun(sc)
+    inp = run.prepare(0)
+    run.store(inp)
+    e0 = int(inp.extend_lens[0].item())
+    assert e0 > 0
+    args_e = (inp.q_ext[:e0], inp.k_new[:e0], inp.v_new[:e0])
+    rpi_e, pre_e, len_e = inp.rpi[:1], inp.prefix_lens[:1], inp.extend_lens[:1]
+    start_e = torch.zeros(1, dtype=torch.int32, device="cuda")
+    oe = pa.ra_extend_attention(*args_e, run.k_pool, run.v_pool, inp.table, rpi_e, pre_e, len_e, start_e, e0,
+                                sc.scale)
+    od = run.decode(inp)
+    torch.cuda.synchronize()
+    ws = torch.empty(pa.ra_decode_workspace_bytes(inp.n_dec, sc.hq, sc.hkv, sc.d, inp.max_seq_len),
+                     dtype=torch.uint8, device="cuda")
+    for rep in range(3):
+        me, md = pa.ra_mixed_attention(*args_e, rpi_e, pre_e, len_e, start_e, e0, inp.q_dec, inp.rpi[inp.n_ext:],
+                                       inp.seq_lens, inp.max_seq_len, run.k_pool, run.v_pool, inp.table, sc.scale,
+                                       workspace=ws)
+        torch.cuda.synchronize()
+        assert torch.equal(me, oe) and torch.equal(md, od), rep
+
+
+def test_mixed_call_workspace_too_small_is_rejected():
+    sc = S.cfg5_mixed_small()
+    log("case: mixed call workspace check")
+    run = ScenarioRun(sc)
+    inp = run.prepare(0)
+    run.store(inp)
+    torch.cuda.synchronize()
+    need = pa.ra_decode_workspace_bytes(inp.n_dec, sc.hq, sc.hkv, sc.d, inp.max_seq_len)
+    assert need > 256  # the batch has split contexts
+    out_d = torch.full_like(inp.q_dec, 7.0)
+    with pytest.raises(pa.RadixAttnError):
+        run.mixed(inp, workspace=torch.empty(need - 256, dtype=torch.uint8, device="cuda"), out_dec=out_d)
+    torch.cuda.synchronize()
+    assert bool((out_d == 7.0).all())
+
+
 def test_mixed_call_rejects_bad_half_without_side_effects():
     sc = S.cfg5_mixed_small()
     log("case: mixed call argument error")
