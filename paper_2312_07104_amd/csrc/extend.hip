@@ -673,6 +673,20 @@ void launch_wide(int64_t items, hipStream_t stream, const __bf16* qp, const __bf
 
 }  // namespace
 
+// Compute units of the current device (cached per device; 256 if the query
+// fails).
+static int ra_device_cus() {
+  static int cached[64] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cached[dev] <= 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+    cached[dev] = n;
+  }
+  return cached[dev];
+}
+
 // Launches the fused-step kernel with 256 (rows = 256) or 128 query rows per
 // work-group for arguments ra_extend_validate accepted.
 static int extend_launch(const void* q, const void* k_new, const void* v_new, int64_t total_tokens,
@@ -747,8 +761,15 @@ extern "C" int ra_extend_attention(const void* q, const void* k_new, const void*
   const int32_t grp = hq / hkv;
   // At least 256 query rows per kv head (new tokens x query heads per kv
   // head): the 256-row configuration; fewer would leave most of its tile
-  // empty, so they take the 128-row one.
-  const int32_t rows = static_cast<int64_t>(max_extend_len) * grp >= 256 ? 256 : 128;
+  // empty, so they take the 128-row one.  The 128-row one also serves a
+  // batch whose 256-row work-groups would not reach one per CU (few requests
+  // and few kv heads, e.g. a head shard): twice the work-groups, so more CUs
+  // share the work.
+  int32_t rows = static_cast<int64_t>(max_extend_len) * grp >= 256 ? 256 : 128;
+  if (rows == 256) {
+    const int64_t items = static_cast<int64_t>(batch) * hkv * ((max_extend_len + 256 / grp - 1) / (256 / grp));
+    if (items < ra_device_cus()) rows = 128;
+  }
   return extend_launch(q, k_new, v_new, total_tokens, k_pool, v_pool, pool_slots, req_to_token, rtt_rows, rtt_stride,
                        req_pool_idx, prefix_lens, extend_lens, extend_start, batch, max_extend_len, hq, hkv, d,
                        scale, out, rows, stream);
