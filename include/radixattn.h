@@ -25,7 +25,10 @@
  * int64.  Node handles are int64 ids; the root is 0; ids are never reused.
  * Every call returns RA_OK or a negative status and never throws; the text of
  * the last error on the calling thread is available from ra_last_error().  A
- * failing call changes nothing.  Query head h uses key/value head
+ * failing call changes nothing, with one exception: when the host runs out of
+ * memory inside a tree or router operation, the call returns RA_ENOMEM and
+ * the handle may be left part-way through it (destroy it).  Query head h uses
+ * key/value head
  * h / (Hq / Hkv) (contiguous groups).
  */
 #ifndef RADIXATTN_H
@@ -43,7 +46,7 @@ extern "C" {
 enum {
   RA_OK = 0,
   RA_EINVAL = -1, /* bad argument, unknown node, counter underflow, bad slot */
-  RA_ENOMEM = -2, /* pool has fewer free slots than asked (host, no effect) */
+  RA_ENOMEM = -2, /* pool has fewer free slots than asked (no effect), or host memory ran out */
   RA_EHIP = -3    /* a HIP launch failed; message holds hipGetErrorString */
 };
 
