@@ -41,6 +41,7 @@
 //     sums come from an MFMA against a ones operand, so numerator and
 //     denominator see the same bf16 P.
 
+#include <atomic>
 #include <type_traits>
 
 #include "device_common.h"
@@ -676,15 +677,15 @@ void launch_wide(int64_t items, hipStream_t stream, const __bf16* qp, const __bf
 // Compute units of the current device (cached per device; 256 if the query
 // fails).
 static int ra_device_cus() {
-  static int cached[64] = {};
+  static std::atomic<int> cached[64] = {};
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
-  if (cached[dev] <= 0) {
-    int n = 0;
+  int n = cached[dev].load(std::memory_order_relaxed);
+  if (n <= 0) {
     if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
-    cached[dev] = n;
+    cached[dev].store(n, std::memory_order_relaxed);
   }
-  return cached[dev];
+  return n;
 }
 
 // Launches the fused-step kernel with 256 (rows = 256) or 128 query rows per
