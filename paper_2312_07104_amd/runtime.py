@@ -361,6 +361,8 @@ def run_data_parallel(sequences, n_workers: int, pool_slots: int, policy: str = 
     (tests check the router against the worker trees there)."""
     if policy not in DP_POLICIES:
         raise ValueError(f"unknown policy {policy!r}; one of {DP_POLICIES}")
+    if n_workers < 1 or commit_every < 1 or slack < 0:
+        raise ValueError("n_workers and commit_every must be >= 1 and slack >= 0")
     from . import Router
 
     seqs = [np.ascontiguousarray(s, dtype=np.int32) for s in sequences]

@@ -81,6 +81,15 @@ def test_native_router_frees_unheld_nodes():
     assert r.num_nodes() == 1 and r.held_tokens(0) == 0 and r.held_tokens(1) == 0
 
 
+def test_data_parallel_argument_errors():
+    seqs = _stream(13, 5)
+    for kw in ({"commit_every": 0}, {"slack": -0.1}):
+        with pytest.raises(ValueError):
+            run_data_parallel(seqs, 2, 100, "affinity", **kw)
+    with pytest.raises(ValueError):
+        run_data_parallel(seqs, 2, 100, "best")
+
+
 def test_router_argument_errors():
     with pytest.raises(pa.RadixAttnError):
         pa.Router(0)
