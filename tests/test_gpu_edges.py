@@ -90,7 +90,9 @@ def test_ragged_extend_tiles(hq, hkv, d):
 def test_extend_kernels_agree_with_oracle(hq, hkv, d):
     """The same batch through the 128-row kernel (query rows per kv head below
     256) and through the 256-row kernel (forced by an inflated, still valid,
-    upper bound on the extend length): both match the oracle."""
+    upper bound on the extend length, large enough that the 256-row launch
+    has at least one work-group per CU; the extra work-groups have no rows
+    and end at once): both match the oracle."""
     log(f"case: both extend kernels hq={hq} hkv={hkv} d={d}")
     grp = hq // hkv
     e_max = max(1, 255 // grp)  # largest extend that stays on the 128-row kernel
@@ -100,8 +102,12 @@ def test_extend_kernels_agree_with_oracle(hq, hkv, d):
     inp = run.prepare(0)
     run.store(inp)
     assert inp.max_extend_len * grp < 256
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    tpb = 256 // grp  # new tokens per 256-row work-group
+    wide = max(inp.max_extend_len, tpb + 1, tpb * -(-cus // (inp.n_ext * hkv)))
+    assert inp.n_ext * hkv * -(-wide // tpb) >= cus
     outs = {}
-    for name, bound in (("narrow", inp.max_extend_len), ("wide", max(inp.max_extend_len, 256 // grp + 1))):
+    for name, bound in (("narrow", inp.max_extend_len), ("wide", wide)):
         outs[name] = pa.ra_extend_attention(
             inp.q_ext, inp.k_new[: inp.total_ext], inp.v_new[: inp.total_ext], run.k_pool, run.v_pool, inp.table,
             inp.rpi[: inp.n_ext], inp.prefix_lens, inp.extend_lens, inp.extend_start, bound, sc.scale)
@@ -323,3 +329,30 @@ def test_mixed_call_rejects_bad_half_without_side_effects():
                               run.k_pool, run.v_pool, inp.table, -1.0, out_dec=out_d)  # negative scale
     torch.cuda.synchronize()
     assert bool((out_d == 7.0).all())
+
+
+@pytest.mark.parametrize("case", range(24))
+def test_random_small_batches(case):
+    """Seeded random batches: group sizes, kv-head counts, head sizes, ragged
+    prefix / extend / decode lengths and split counts that the fixed cases do
+    not list.  Every output against the oracle; where the batch has both
+    halves, the mixed call equals the separate calls bit for bit."""
+    rng = np.random.default_rng(9000 + case)
+    grp = int(rng.choice([1, 2, 4, 8, 16]))
+    hkv = int(rng.choice([1, 2, 4, 8]))
+    hkv = max(1, min(hkv, 64 // grp))
+    hq, d = grp * hkv, int(rng.choice([64, 128]))
+    n_ext = int(rng.integers(0, 5))
+    n_dec = int(rng.integers(0 if n_ext else 1, 6))
+    extend = [(int(rng.integers(0, 700)), int(rng.integers(1, 200))) for _ in range(n_ext)]
+    decode = [int(rng.integers(1, 3000)) for _ in range(n_dec)]
+    num_splits = int(rng.choice([0, 0, 1, 2, 5, 17]))
+    pool = sum(p + e for p, e in extend) + sum(decode) + 256
+    log(f"case: random {case} hq={hq} hkv={hkv} d={d} extend={extend} decode={decode} splits={num_splits}")
+    sc = _scenario(f"random{case}", hq, hkv, d, pool, extend=extend, decode=decode, seed=300 + case)
+    run, inp, oe, od = _run(sc, num_splits=num_splits)
+    _check_all(run, inp, oe, od, f"random {case}")
+    if n_ext and n_dec:
+        me, md = run.mixed(inp, num_splits=num_splits)
+        torch.cuda.synchronize()
+        assert torch.equal(me, oe) and torch.equal(md, od)
