@@ -4,7 +4,10 @@
 // long (evaluation, section 6.2); it is bound by HBM bandwidth, so the design
 // goal is a steady stream of gathered 256-byte K/V rows.
 //
-// Work item = (request, kv head, KV chunk); one wave per item.
+// Work item = (request, kv head, KV chunk); one wave per item.  Two
+// partial-pass kernels share the item layout, the per-tile arithmetic and the
+// outputs: decode_partial_vr_kernel (D = 128) stages the gathered rows in
+// registers, decode_partial_kernel (D = 64) copies them straight into LDS:
 //   * Gather: every 32-token tile's K and V rows are copied HBM -> LDS with
 //     direct-to-LDS loads (global_load_lds_dwordx4), kNS tiles deep, no VGPR
 //     staging; the slot indices travel the same way one tile further ahead,
@@ -265,6 +268,233 @@ __global__ __launch_bounds__(64) void decode_partial_kernel(
   }
 }
 
+// Decode partial pass with register staging (D = 128).  The kernel above
+// copies K and V straight into LDS, so its tiles in flight are bounded twice
+// (measured with D = 128):
+// a wave's vector-memory counter holds 63 loads (three 16 KB tiles of 1 KB
+// copies), and LDS holds two such rings per CU, 96 KB in flight per CU in
+// all.  Decode is bound by exactly that: with one of the two waves per CU
+// removed it runs at 0.54-0.65x.  Here each tile's rows are read with
+// ordinary vector loads into registers: K straight into the MFMA A-operand
+// layout (16 bytes of one row per lane, the same lanes and rows the LDS
+// kernel reads), V in the copy layout, written to a single 8 KB LDS tile just
+// before its PV step (V^T needs the transposing LDS read).  Registers hold
+// the NP tiles in flight, the compiler tracks every load (no hand-counted
+// waits), and LDS no longer limits the waves per CU.  Per tile the arithmetic
+// (operands, accumulation order, maximum rule, rounding) is that of
+// decode_partial_kernel, so the two write bit-identical partial outputs.
+template <int NP>
+__global__ __launch_bounds__(64) void decode_partial_vr_kernel(
+    const __bf16* __restrict__ q, const __bf16* __restrict__ k_pool, const __bf16* __restrict__ v_pool,
+    int64_t pool_slots, const int32_t* __restrict__ rtt, int64_t rtt_rows, int64_t rtt_stride,
+    const int32_t* __restrict__ req_pool_idx, const int32_t* __restrict__ seq_lens, int32_t batch,
+    int32_t hkv, int32_t grp, int32_t chunk_len, int32_t max_splits, int32_t max_len, float scale_log2,
+    float* __restrict__ ws_o, float* __restrict__ ws_lse, __bf16* __restrict__ out) {
+  constexpr int D = 128;
+  constexpr int TILE = kTile;
+  constexpr int KS = D / 32;
+  constexpr int DB = D / 16;
+  constexpr int NB = TILE / 16;
+  constexpr int GROUP_B = TILE * 64;
+  constexpr int TILE_B = KS * GROUP_B;
+  __shared__ __align__(16) unsigned char v_lds[TILE_B];
+
+  const int64_t n_items = static_cast<int64_t>(hkv) * max_splits * batch;
+  const int64_t per_xcd = (n_items + 7) / 8;
+  const int64_t item = static_cast<int64_t>(blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
+  if (item >= n_items) return;
+  const int g = static_cast<int>(item / (static_cast<int64_t>(max_splits) * batch));
+  const int rem = static_cast<int>(item % (static_cast<int64_t>(max_splits) * batch));
+  const int split = rem / batch;
+  const int b = rem % batch;
+  const int L = min(seq_lens[b], max_len);
+  if (L <= 0) return;
+  const int n_splits = (L + chunk_len - 1) / chunk_len;
+  if (split >= n_splits) return;
+  const int t_begin = split * chunk_len;
+  const int t_end = min(L, t_begin + chunk_len);
+  int64_t rrow = req_pool_idx[b];
+  rrow = (rrow >= 0 && rrow < rtt_rows) ? rrow : 0;
+  const int32_t* trow = rtt + rrow * rtt_stride;
+  const int hq = hkv * grp;
+  const int n_tiles = (t_end - t_begin + TILE - 1) / TILE;
+
+  const int lane = threadIdx.x;
+  const int c = lane & 15;
+  const int g4 = lane >> 4;
+  // Rows of a tile this lane loads.  K: A-operand row c of block bb is token
+  // 8 (c >> 2) + 4 bb + (c & 3) (so accumulator row group g4 holds tokens
+  // 8 g4 .. 8 g4 + 7, P^T's k slots in order); the lane's 16 bytes of each
+  // k-step are d = 32 ks + 8 g4 .. + 7.  V: copy row u = 16 rb + (lane >> 2),
+  // logical piece (lane & 3) ^ swizzle(u) of each 64-byte piece group, stored
+  // at LDS byte pg * GROUP_B + rb * 1024 + 16 lane (the LDS kernel's layout).
+  int kr[NB];
+#pragma unroll
+  for (int bb = 0; bb < NB; ++bb) kr[bb] = 8 * (c >> 2) + 4 * bb + (c & 3);
+  int vu[2];
+  uint32_t vpc[2];
+#pragma unroll
+  for (int rb = 0; rb < 2; ++rb) {
+    vu[rb] = 16 * rb + (lane >> 2);
+    vpc[rb] = 16u * static_cast<uint32_t>((lane & 3) ^ ra_kv_swz(vu[rb]));
+  }
+  const uint32_t row_bytes = static_cast<uint32_t>(hkv) * D * 2;
+  const unsigned char* kbase = reinterpret_cast<const unsigned char*>(k_pool) + g * D * 2 + 16 * g4;
+  const unsigned char* vbase = reinterpret_cast<const unsigned char*>(v_pool) + g * D * 2;
+  const uint32_t smax = static_cast<uint32_t>(pool_slots - 1);
+
+  // Slot index of token (lane & 31) of a tile; padding repeats the last token.
+  auto load_idx = [&](int tile) -> int32_t {
+    const int pos = min(t_begin + tile * TILE + (lane & (TILE - 1)), t_end - 1);
+    return trow[pos];
+  };
+  uint4 kbuf[NP][NB][KS];
+  uint4 vbuf[NP][2][KS];
+  int32_t ibuf[NP];
+  auto load_tile = [&](int j, int32_t idx) {
+#pragma unroll
+    for (int bb = 0; bb < NB; ++bb) {
+      const uint32_t slot = min(static_cast<uint32_t>(__shfl(idx, kr[bb])), smax);  // negative -> clamped
+      const unsigned char* p = kbase + static_cast<uint64_t>(slot) * row_bytes;
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) kbuf[j][bb][ks] = ra_ld16(p + 64 * ks);
+    }
+#pragma unroll
+    for (int rb = 0; rb < 2; ++rb) {
+      const uint32_t slot = min(static_cast<uint32_t>(__shfl(idx, vu[rb])), smax);
+      const unsigned char* p = vbase + static_cast<uint64_t>(slot) * row_bytes + vpc[rb];
+#pragma unroll
+      for (int pg = 0; pg < KS; ++pg) vbuf[j][rb][pg] = ra_ld16(p + 64 * pg);
+    }
+  };
+
+  bf16x8_t qt[KS];
+  {
+    const bool has = c < grp;
+    const __bf16* qp = q + (static_cast<int64_t>(b) * hq + g * grp + (has ? c : 0)) * D + 8 * g4;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+      qt[ks] = __builtin_bit_cast(bf16x8_t, has ? ra_ld16(qp + 32 * ks) : make_uint4(0, 0, 0, 0));
+  }
+
+#pragma unroll
+  for (int j = 0; j < NP; ++j) ibuf[j] = load_idx(j);
+#pragma unroll
+  for (int j = 0; j < NP; ++j)
+    if (j < n_tiles) load_tile(j, ibuf[j]);
+#pragma unroll
+  for (int j = 0; j < NP; ++j) ibuf[j] = load_idx(j + NP);
+
+  f32x4_t o[DB];
+#pragma unroll
+  for (int i = 0; i < DB; ++i) o[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  float m_run = -INFINITY;
+  float l_run = 0.f;
+  const int vr0 = 8 * g4 + (c >> 2);
+  uint32_t voff[2];
+#pragma unroll
+  for (int e = 0; e < 2; ++e) voff[e] = vr0 * 64 + 16 * ((2 * e + ((c & 3) >> 1)) ^ ra_kv_swz(vr0)) + 8 * (c & 1);
+
+  for (int tb = 0; tb < n_tiles; tb += NP) {
+#pragma unroll
+    for (int j = 0; j < NP; ++j) {
+      const int t = tb + j;
+      if (t < n_tiles) {
+        // V(t) into the LDS tile (the previous tile's transposed reads were
+        // consumed by its PV MFMAs, so the tile is free).
+#pragma unroll
+        for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+          for (int pg = 0; pg < KS; ++pg)
+            *reinterpret_cast<uint4*>(v_lds + pg * GROUP_B + rb * 1024 + 16 * lane) = vbuf[j][rb][pg];
+        const int t0 = t_begin + t * TILE;
+        f32x4_t sacc[NB];
+#pragma unroll
+        for (int bb = 0; bb < NB; ++bb) {
+          sacc[bb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int ks = 0; ks < KS; ++ks)
+            sacc[bb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, kbuf[j][bb][ks]),
+                                                                qt[ks], sacc[bb], 0, 0, 0);
+        }
+        // Slot j is consumed: refill it with tile t + NP, and its index
+        // register with the indices of tile t + 2 NP.
+        if (t + NP < n_tiles) load_tile(j, ibuf[j]);
+        ibuf[j] = load_idx(t + 2 * NP);
+
+        if (t0 + TILE > t_end) {
+#pragma unroll
+          for (int bb = 0; bb < NB; ++bb)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              const int tok = t0 + 8 * g4 + 4 * bb + i;
+              if (tok >= t_end) sacc[bb][i] = -INFINITY;
+            }
+        }
+        float mt = fmaxf(fmaxf(fmaxf(sacc[0][0], sacc[0][1]), fmaxf(sacc[0][2], sacc[0][3])),
+                         fmaxf(fmaxf(sacc[1][0], sacc[1][1]), fmaxf(sacc[1][2], sacc[1][3])));
+        mt = ra_max_across_rows(mt);
+        if (__builtin_amdgcn_ballot_w64((mt - m_run) * scale_log2 > 8.f) != 0) {
+          const float m_new = fmaxf(m_run, mt);
+          const float alpha = ra_exp2((m_run - m_new) * scale_log2);
+          l_run *= alpha;
+#pragma unroll
+          for (int i = 0; i < DB; ++i) o[i] *= alpha;
+          m_run = m_new;
+        }
+        const float mb = -m_run * scale_log2;
+        float p[8];
+#pragma unroll
+        for (int bb = 0; bb < NB; ++bb)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            p[4 * bb + i] = ra_exp2(__builtin_fmaf(sacc[bb][i], scale_log2, mb));
+            l_run += p[4 * bb + i];
+          }
+        uint4 pw;
+        pw.x = ra_pack_bf16x2(p[0], p[1]);
+        pw.y = ra_pack_bf16x2(p[2], p[3]);
+        pw.z = ra_pack_bf16x2(p[4], p[5]);
+        pw.w = ra_pack_bf16x2(p[6], p[7]);
+        const bf16x8_t pt = __builtin_bit_cast(bf16x8_t, pw);
+#pragma unroll
+        for (int db = 0; db < DB; ++db) {
+          const unsigned char* vb = v_lds + voff[db & 1] + (db >> 1) * GROUP_B;
+          const bf16x4_t lo =
+              __builtin_amdgcn_ds_read_tr16_b64_v4bf16((__attribute__((address_space(3))) bf16x4_t*)(vb));
+          const bf16x4_t hi =
+              __builtin_amdgcn_ds_read_tr16_b64_v4bf16((__attribute__((address_space(3))) bf16x4_t*)(vb + 4 * 64));
+          const bf16x8_t a = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+          o[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pt, o[db], 0, 0, 0);
+        }
+      }
+    }
+  }
+
+  const float l_tot = ra_sum_across_rows(l_run);
+  if (c >= grp) return;
+  const int head = g * grp + c;
+  const float inv = 1.f / l_tot;
+  if (n_splits == 1) {
+    __bf16* op = out + (static_cast<int64_t>(b) * hq + head) * D + 4 * g4;
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+      uint2 w;
+      w.x = ra_pack_bf16x2(o[db][0] * inv, o[db][1] * inv);
+      w.y = ra_pack_bf16x2(o[db][2] * inv, o[db][3] * inv);
+      *reinterpret_cast<uint2*>(op + 16 * db) = w;
+    }
+  } else {
+    const int64_t pidx = (static_cast<int64_t>(b) * hq + head) * max_splits + split;
+    float* wp = ws_o + pidx * D + 4 * g4;
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+      *reinterpret_cast<float4*>(wp + 16 * db) =
+          make_float4(o[db][0] * inv, o[db][1] * inv, o[db][2] * inv, o[db][3] * inv);
+    if (g4 == 0) ws_lse[pidx] = m_run * scale_log2 + __log2f(l_tot);
+  }
+}
+
 // Merges the chunks of one (request, head): weights 2^(lse_i - max lse).
 template <int D>
 __global__ __launch_bounds__(64) void decode_combine_kernel(const float* __restrict__ ws_o,
@@ -388,15 +618,16 @@ extern "C" int ra_decode_attention(const void* q, const void* k_pool, const void
   hipLaunchKernelGGL((decode_partial_kernel<DD, NN>), dim3(static_cast<uint32_t>(grid)), dim3(64), 0, stream, \
                      qp, kp, vp, pool_slots, req_to_token, rtt_rows, rtt_stride, req_pool_idx, seq_lens, batch, hkv, \
                      grp, chunk, max_splits, max_seq_len, scale_log2, ws_o, ws_lse, op)
-  // 32-key tiles.  D = 128: with chunks of 4096 tokens a wave streams long
-  // enough that a four-tile ring per wave (66 KB of LDS, two waves per CU)
-  // wins; with shorter chunks, fewer items per CU or short contexts, a
-  // three-tile ring (50 KB, three waves per CU) hides more latency
-  // (measured: 7-16% faster on 256-request chat batches and on head shards,
-  // 9% slower on 512 requests of 1k-16k tokens).  D = 64: three tiles.
+  // D = 128: register staging, two tiles in flight per wave, four waves per
+  // CU (measured against the LDS-copy kernel with a three- or four-tile
+  // ring: 7% faster on 512 requests of 1k-16k tokens, 8% on 256-request chat
+  // batches, 11% on the branching decode, 2-7% on head shards; three or four
+  // tiles in flight per wave are no faster).  D = 64: the LDS-copy kernel,
+  // three-tile ring.
   if (d == 128) {
-    if (chunk >= 4096) RA_LAUNCH_DECODE(128, 4);
-    else RA_LAUNCH_DECODE(128, 3);
+    hipLaunchKernelGGL((decode_partial_vr_kernel<2>), dim3(static_cast<uint32_t>(grid)), dim3(64), 0, stream, qp, kp,
+                       vp, pool_slots, req_to_token, rtt_rows, rtt_stride, req_pool_idx, seq_lens, batch, hkv, grp,
+                       chunk, max_splits, max_seq_len, scale_log2, ws_o, ws_lse, op);
   } else {
     RA_LAUNCH_DECODE(64, 3);
   }
