@@ -11,7 +11,10 @@ heads, 8 kv heads, head dim 128): 32 extend requests (cached prefix
 U[1024, 8192], extend U[256, 2048]) and 512 decode requests (context
 U[1024, 16384]) over a 4,194,304-slot pool, tables built by ~100k tree calls.
 
-Prints one JSON line.  The headline loop runs the steps back to back (the
+Prints one JSON line.  Before anything is timed, untimed steps run for
+--clock-warmup seconds (the GPU's clocks ramp up over the first tens of
+milliseconds of sustained load), then the W warm-up steps.  The headline loop
+runs the steps back to back (the
 mixed call overlaps extend and decode on two streams).  A second loop runs the
 same work one kernel at a time, each step after a 1 GiB write that evicts L2
 and the Infinity Cache (cold caches), with HIP events recorded on the stream
@@ -192,6 +195,9 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--clock-warmup", type=float, default=1.0,
+                    help="seconds of untimed steps before the W warm-up steps: the GPU's clocks ramp up over "
+                         "the first tens of milliseconds of sustained load")
     ap.add_argument("--workload", default="mixed")
     ap.add_argument("--phase", type=int, default=0,
                     help="batch of the workload to time; earlier batches run and finish first (their new tokens "
@@ -255,6 +261,12 @@ def main():
             run.decode(inp, workspace=ws_t, out=out_d)
         ev[3].record(stream)
 
+    clock_steps = 0
+    t_cw = time.perf_counter()
+    while time.perf_counter() - t_cw < args.clock_warmup:
+        step()
+        torch.cuda.synchronize()
+        clock_steps += 1
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
@@ -272,9 +284,12 @@ def main():
         step_sequential(events[i])
     torch.cuda.synchronize()
     ms_seq = float(np.mean([e[0].elapsed_time(e[3]) for e in events]))
-    t_store = float(np.mean([e[0].elapsed_time(e[1]) for e in events]))
-    t_ext = float(np.mean([e[1].elapsed_time(e[2]) for e in events]))
-    t_dec = float(np.mean([e[2].elapsed_time(e[3]) for e in events]))
+    per_step = {"store_kv": [e[0].elapsed_time(e[1]) for e in events],
+                "extend": [e[1].elapsed_time(e[2]) for e in events],
+                "decode": [e[2].elapsed_time(e[3]) for e in events]}
+    t_store = float(np.mean(per_step["store_kv"]))
+    t_ext = float(np.mean(per_step["extend"]))
+    t_dec = float(np.mean(per_step["decode"]))
 
     kernels = {
         "store_kv": {"ms": t_store, "tokens": int(n_new)},
@@ -306,6 +321,10 @@ def main():
     first, second = (extend_roof, decode_roof) if inp.n_ext and t_ext >= t_dec else (decode_roof, extend_roof)
     roof = first()
     other = second() if (kernels["decode"] if second is decode_roof else kernels["extend"]) else None
+    for name, k in kernels.items():
+        if k:
+            k["ms_median"] = float(np.median(per_step[name]))
+            k["ms_min"] = float(np.min(per_step[name]))
     for r in (roof, other):
         if r:
             r["frac"] = r["achieved"] / r["peak"]
@@ -331,6 +350,7 @@ def main():
                    "sum_extend_tokens": inp.total_ext, "sum_decode_context": work["sum_l"],
                    "history_requests": sc.history_len, "tree_calls": run.history_ops,
                    "hit_rate": inp.plan.hit_rate, "parallelism": "none (1 GPU)"},
+        "clock_warmup": {"seconds": args.clock_warmup, "steps": clock_steps},
         "ms_per_step_sequential_cold": ms_seq,
         "roofline": roof,
         "roofline_other": other,
