@@ -342,8 +342,9 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void extend_kernel(
           else s_mfma_acc(s[bb][j], a, qT[j][ks]);
         }
       }
-    // let the last MFMAs retire before the VALU reads S^T
-    asm volatile("s_nop 7\n\ts_nop 7" : "+v"(s[0][0]), "+v"(s[1][kQB - 1]));
+    // let the last MFMAs retire before the VALU reads S^T (every block is an
+    // operand, so no MFMA writing one can be scheduled past the nops)
+    asm volatile("s_nop 7\n\ts_nop 7" : "+v"(s[0][0]), "+v"(s[0][1]), "+v"(s[1][0]), "+v"(s[1][1]));
   };
 
   // Maximum of one half's scores per query column (this lane's 8 keys).
