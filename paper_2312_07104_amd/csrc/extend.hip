@@ -9,7 +9,9 @@
 // head share every K/V tile.  Waves of 32 query rows (two 16-column MFMA
 // blocks), two waves per SIMD: eight waves and 256 rows per work-group with
 // 64-key tiles (one work-group per CU), or four waves and 128 rows with
-// 32-key tiles (two per CU) for requests with fewer rows.
+// 32-key tiles (two per CU) for requests with fewer rows.  Work items start
+// longest first (ra_lpt_item), so batches that fill the chip only a few
+// times over do not end on their longest items.
 //   * K/V tiles arrive by direct-to-LDS copies (global_load_lds_dwordx4: a
 //     prefix row is gathered through the request's slot-table row, a new
 //     token's row read from k_new / v_new) into a four-stage ring, two tiles
@@ -72,6 +74,95 @@ __device__ __forceinline__ void s_mfma_acc(f32x4_t& s, const bf16x8_t& a, const 
   asm("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0" : "+v"(s) : "v"(a), "a"(qa));
 }
 
+// Requests above this batch size keep the static item order (the ranking
+// below is quadratic in the batch and its scratch lives in the K/V ring).
+constexpr int kLptMaxBatch = 1024;  // 7 * 1024 + 2 words fit every configuration's ring
+
+// Work item of block k in longest-first order.  A unit is (request, query
+// tile).  Units are ordered by their request's key count P + E, longest
+// first (ties by request index), and within a request by query tile, the
+// last (longest) tile first.  Block k takes unit k / hkv of kv head
+// k % hkv.  The dispatcher starts blocks in index order and deals them to
+// the XCDs round-robin, so every XCD runs its share longest-first, and with
+// 8 | hkv each XCD keeps whole kv heads (its L2 sees their rows only).  A
+// static order would leave the longest items for the end when a batch fills
+// the chip only a few times over (short extends, head shards).  Every
+// thread of the work-group takes part; `scratch` holds 7 * batch + 2 words of
+// LDS.  The request's own arguments (start, E, P and table row, as passed)
+// come back through `req_args`, read once for the whole batch.  Returns
+// false when block k has no unit.
+__device__ bool ra_lpt_item(int32_t* scratch, int64_t k, int32_t hkv, int32_t batch, int32_t tpb,
+                            const int32_t* __restrict__ req_pool_idx, const int32_t* __restrict__ prefix_lens,
+                            const int32_t* __restrict__ extend_lens, const int32_t* __restrict__ extend_start,
+                            int64_t total_tokens, int64_t rtt_stride, int& g, int& b, int& qt,
+                            int32_t (&req_args)[4]) {
+  int32_t* args = scratch;              // [batch][4] start, E, P, table row as passed (16-byte entries)
+  int32_t* cost = scratch + 4 * batch;  // [batch] key count of the request's units, -1 if none
+  int32_t* nun = scratch + 5 * batch;   // [batch] units of the request; then units by rank
+  int32_t* ord = scratch + 6 * batch;   // [batch] request at each rank
+  int32_t* found = scratch + 7 * batch; // [2] request and unit offset of this block
+  const int tid = threadIdx.x, nt = blockDim.x;
+  if (tid == 0) found[0] = -1;
+  for (int t = tid; t < batch; t += nt) {
+    const int32_t st = extend_start[t], el = extend_lens[t], pl = prefix_lens[t], rp = req_pool_idx[t];
+    *reinterpret_cast<int4*>(&args[4 * t]) = make_int4(st, el, pl, rp);
+    const int64_t e = (st < 0 || st > total_tokens) ? 0 : min<int64_t>(el, total_tokens - st);
+    const int64_t p = min<int64_t>(max(pl, 0), rtt_stride);
+    const int64_t nu = e > 0 ? (e + tpb - 1) / tpb : 0;
+    nun[t] = static_cast<int32_t>(nu);
+    cost[t] = nu > 0 ? static_cast<int32_t>(min<int64_t>(p + e, INT32_MAX)) : -1;
+  }
+  __syncthreads();
+  int32_t rk[4], nu_own[4];  // batch <= kLptMaxBatch <= 4 * blockDim.x
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int t = tid + i * nt;
+    rk[i] = -1;
+    if (t < batch) {
+      const int32_t c = cost[t];
+      int rank = 0;
+      for (int s2 = 0; s2 < batch; ++s2) {
+        const int32_t cs = cost[s2];
+        rank += (cs > c) | ((cs == c) & (s2 < t));
+      }
+      rk[i] = rank;
+      nu_own[i] = nun[t];
+    }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    if (rk[i] >= 0) {
+      ord[rk[i]] = tid + i * nt;
+      nun[rk[i]] = nu_own[i];  // nun now holds the unit counts in rank order
+    }
+  }
+  __syncthreads();
+  const int64_t r = k / hkv;
+  for (int j = tid; j < batch; j += nt) {
+    int64_t before = 0;
+    for (int i = 0; i < j; ++i) before += nun[i];
+    if (r >= before && r < before + nun[j]) {
+      found[0] = ord[j];
+      found[1] = static_cast<int32_t>(nun[j] - 1 - (r - before));
+    }
+  }
+  __syncthreads();
+  const int req = found[0];
+  const int tile = found[1];
+  if (req >= 0) {
+    const int4 a = *reinterpret_cast<const int4*>(&args[4 * req]);
+    req_args[0] = a.x, req_args[1] = a.y, req_args[2] = a.z, req_args[3] = a.w;
+  }
+  // the scratch is the K/V ring, which the copies overwrite next
+  __syncthreads();
+  if (req < 0) return false;
+  g = static_cast<int>(k % hkv);
+  b = req;
+  qt = tile;
+  return true;
+}
+
 // WAVES waves of 32 query rows per work-group, BN keys per K/V tile (64:
 // two 32-key halves per tile; 32: one).  <D, 8, 64>: 256 rows, one
 // work-group per CU; <D, 4, 32>: 128 rows, two work-groups per CU (65 KB of
@@ -83,7 +174,7 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void extend_kernel(
     int64_t pool_slots, const int32_t* __restrict__ rtt, int64_t rtt_rows, int64_t rtt_stride,
     const int32_t* __restrict__ req_pool_idx, const int32_t* __restrict__ prefix_lens,
     const int32_t* __restrict__ extend_lens, const int32_t* __restrict__ extend_start, int32_t batch,
-    int32_t hkv, int32_t grp, int32_t n_qtiles, float scale_log2, __bf16* __restrict__ out) {
+    int32_t hkv, int32_t grp, int32_t n_qtiles, int32_t lpt, float scale_log2, __bf16* __restrict__ out) {
   constexpr int kWaves = WAVES;
   constexpr int kBN = BN;
   constexpr int kBM = 32 * WAVES;             // query rows per work-group
@@ -100,28 +191,40 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void extend_kernel(
   // one index copy moves 64 words (rows beyond the tile are never read)
   __shared__ __align__(16) int32_t idx_lds[kRing][64];
 
-  // Work-groups go to the 8 XCDs round-robin (block i -> XCD i % 8); each XCD
-  // takes a contiguous eighth of the (kv head, request, query tile) order, so
-  // the work-groups on one XCD share K/V rows through its L2.
-  const int64_t n_items = static_cast<int64_t>(hkv) * batch * n_qtiles;
-  const int64_t per_xcd = (n_items + 7) / 8;
-  const int64_t item = static_cast<int64_t>(blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
-  if (item >= n_items) return;
-  const int g = static_cast<int>(item / (static_cast<int64_t>(batch) * n_qtiles));
-  const int rem = static_cast<int>(item % (static_cast<int64_t>(batch) * n_qtiles));
-  const int b = rem / n_qtiles;
-  const int qt = n_qtiles - 1 - rem % n_qtiles;
+  // Work-groups go to the 8 XCDs round-robin (block i -> XCD i % 8).  Either
+  // order below keeps the blocks of one kv head together on an XCD where it
+  // can, so they share K/V rows through its L2.
   const int tpb = kBM / grp;  // new tokens per tile
+  const int64_t n_items = static_cast<int64_t>(hkv) * batch * n_qtiles;
+  int g, b, qt;
+  int32_t req_args[4];  // extend_start, extend_lens, prefix_lens, req_pool_idx of request b
+  if (lpt) {
+    if (!ra_lpt_item(reinterpret_cast<int32_t*>(kv_lds), blockIdx.x, hkv, batch, tpb, req_pool_idx, prefix_lens,
+                     extend_lens, extend_start, total_tokens, rtt_stride, g, b, qt, req_args))
+      return;
+  } else {
+    // Static order: XCD i % 8 takes a contiguous eighth of the (kv head,
+    // request, query tile) order.
+    const int64_t per_xcd = (n_items + 7) / 8;
+    const int64_t item = static_cast<int64_t>(blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
+    if (item >= n_items) return;
+    g = static_cast<int>(item / (static_cast<int64_t>(batch) * n_qtiles));
+    const int rem = static_cast<int>(item % (static_cast<int64_t>(batch) * n_qtiles));
+    b = rem / n_qtiles;
+    qt = n_qtiles - 1 - rem % n_qtiles;
+    req_args[0] = extend_start[b], req_args[1] = extend_lens[b], req_args[2] = prefix_lens[b];
+    req_args[3] = req_pool_idx[b];
+  }
 
-  const int64_t start = extend_start[b];
-  int64_t E = extend_lens[b];
+  const int64_t start = req_args[0];
+  int64_t E = req_args[1];
   if (start < 0 || start > total_tokens) return;
   E = min(E, total_tokens - start);
   const int tok0 = qt * tpb;
   if (E <= 0 || tok0 >= E) return;
   const int tok_end = static_cast<int>(min<int64_t>(E, tok0 + tpb));
-  const int P = static_cast<int>(min<int64_t>(max(prefix_lens[b], 0), rtt_stride));
-  int64_t rrow = req_pool_idx[b];
+  const int P = static_cast<int>(min<int64_t>(max(req_args[2], 0), rtt_stride));
+  int64_t rrow = req_args[3];
   rrow = (rrow >= 0 && rrow < rtt_rows) ? rrow : 0;
   const int32_t* trow = rtt + rrow * rtt_stride;
   const int kend = P + tok_end;
@@ -666,11 +769,11 @@ template <int D, int WAVES, int BN>
 void launch_wide(int64_t items, hipStream_t stream, const __bf16* qp, const __bf16* knp, const __bf16* vnp,
                  int64_t total_tokens, const __bf16* kp, const __bf16* vp, int64_t pool_slots, const int32_t* rtt,
                  int64_t rtt_rows, int64_t rtt_stride, const int32_t* rpi, const int32_t* pl, const int32_t* el,
-                 const int32_t* es, int32_t batch, int32_t hkv, int32_t grp, int32_t n_qtiles, float scale_log2,
+                 const int32_t* es, int32_t batch, int32_t hkv, int32_t grp, int32_t n_qtiles, int32_t lpt, float scale_log2,
                  __bf16* op) {
   hipLaunchKernelGGL((extend_kernel<D, WAVES, BN>), dim3(static_cast<uint32_t>(items)), dim3(WAVES * 64), 0,
                      stream, qp, knp, vnp, total_tokens, kp, vp, pool_slots, rtt, rtt_rows, rtt_stride, rpi, pl, el,
-                     es, batch, hkv, grp, n_qtiles, scale_log2, op);
+                     es, batch, hkv, grp, n_qtiles, lpt, scale_log2, op);
 }
 
 }  // namespace
@@ -710,9 +813,10 @@ static int extend_launch(const void* q, const void* k_new, const void* v_new, in
   auto* vp = static_cast<const __bf16*>(v_pool);
   auto* op = static_cast<__bf16*>(out);
   const int32_t nq = static_cast<int32_t>(n_qtiles);
+  const int32_t lpt = batch <= kLptMaxBatch ? 1 : 0;
 #define RA_WIDE_LAUNCH(DD, W, B)                                                                                   \
   launch_wide<DD, W, B>(items, stream, qp, knp, vnp, total_tokens, kp, vp, pool_slots, req_to_token, rtt_rows,     \
-                        rtt_stride, req_pool_idx, prefix_lens, extend_lens, extend_start, batch, hkv, grp, nq,    \
+                        rtt_stride, req_pool_idx, prefix_lens, extend_lens, extend_start, batch, hkv, grp, nq, lpt, \
                         scale_log2, op)
   if (rows == 256) {
     if (d == 128) RA_WIDE_LAUNCH(128, 8, 64);
