@@ -31,6 +31,22 @@ namespace {
 
 constexpr int kTile = 32;  // tokens per tile (two 16-row MFMA blocks)
 
+// Work item of block k: unit k / hkv of kv head k % hkv, units ordered
+// (split, request).  The dispatcher deals blocks to the 8 XCDs round-robin,
+// so with 8 kv heads each XCD serves one kv head (its requests in flight
+// share prefix chunks through its L2), and with fewer kv heads the XCDs that
+// share a kv head take its units in turn: every XCD gets the same mix of
+// requests, not a contiguous run of them.  Returns false past the last item.
+__device__ __forceinline__ bool ra_decode_item(int64_t k, int32_t hkv, int32_t max_splits, int32_t batch, int& g,
+                                               int& split, int& b) {
+  const int64_t unit = k / hkv;
+  if (unit >= static_cast<int64_t>(max_splits) * batch) return false;
+  g = static_cast<int>(k % hkv);
+  split = static_cast<int>(unit / batch);
+  b = static_cast<int>(unit % batch);
+  return true;
+}
+
 // LDS tile layout (K and V alike): [piece group pg = D/32][token row][4
 // pieces of 16 B], pieces swizzled by ra_kv_swz (conflict-free operand reads,
 // every read one per-lane offset plus an immediate).
@@ -73,18 +89,8 @@ __global__ __launch_bounds__(64) void decode_partial_kernel(
   __shared__ __align__(16) unsigned char kv_lds[NS][2][TILE_B];
   __shared__ __align__(16) int32_t idx_lds[RING][64];
 
-  // Work items ordered (kv head, split, request); each XCD (blocks go to the
-  // 8 XCDs round-robin) takes a contiguous eighth, so one XCD serves one kv
-  // head (with 8 kv heads) and the requests in flight on it share prefix
-  // chunks through its L2.
-  const int64_t n_items = static_cast<int64_t>(hkv) * max_splits * batch;
-  const int64_t per_xcd = (n_items + 7) / 8;
-  const int64_t item = static_cast<int64_t>(blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
-  if (item >= n_items) return;
-  const int g = static_cast<int>(item / (static_cast<int64_t>(max_splits) * batch));
-  const int rem = static_cast<int>(item % (static_cast<int64_t>(max_splits) * batch));
-  const int split = rem / batch;
-  const int b = rem % batch;
+  int g, split, b;
+  if (!ra_decode_item(blockIdx.x, hkv, max_splits, batch, g, split, b)) return;
   const int L = min(seq_lens[b], max_len);  // host bound (<= rtt_stride, <= chunk_len * max_splits)
   if (L <= 0) return;
   const int n_splits = (L + chunk_len - 1) / chunk_len;
@@ -299,14 +305,8 @@ __global__ __launch_bounds__(64) void decode_partial_vr_kernel(
   constexpr int TILE_B = KS * GROUP_B;
   __shared__ __align__(16) unsigned char v_lds[TILE_B];
 
-  const int64_t n_items = static_cast<int64_t>(hkv) * max_splits * batch;
-  const int64_t per_xcd = (n_items + 7) / 8;
-  const int64_t item = static_cast<int64_t>(blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
-  if (item >= n_items) return;
-  const int g = static_cast<int>(item / (static_cast<int64_t>(max_splits) * batch));
-  const int rem = static_cast<int>(item % (static_cast<int64_t>(max_splits) * batch));
-  const int split = rem / batch;
-  const int b = rem % batch;
+  int g, split, b;
+  if (!ra_decode_item(blockIdx.x, hkv, max_splits, batch, g, split, b)) return;
   const int L = min(seq_lens[b], max_len);
   if (L <= 0) return;
   const int n_splits = (L + chunk_len - 1) / chunk_len;
