@@ -76,7 +76,7 @@ __device__ __forceinline__ void s_mfma_acc(f32x4_t& s, const bf16x8_t& a, const 
 
 // Requests above this batch size keep the static item order (the ranking
 // below is quadratic in the batch and its scratch lives in the K/V ring).
-constexpr int kLptMaxBatch = 1024;  // 7 * 1024 + 2 words fit every configuration's ring
+constexpr int kLptMaxBatch = 1024;  // 7 * 1024 + 10 words fit every configuration's ring
 
 // Work item of block k in longest-first order.  A unit is (request, query
 // tile).  Units are ordered by their request's key count P + E, longest
@@ -87,23 +87,31 @@ constexpr int kLptMaxBatch = 1024;  // 7 * 1024 + 2 words fit every configuratio
 // 8 | hkv each XCD keeps whole kv heads (its L2 sees their rows only).  A
 // static order would leave the longest items for the end when a batch fills
 // the chip only a few times over (short extends, head shards).  Every
-// thread of the work-group takes part; `scratch` holds 7 * batch + 2 words of
-// LDS.  The request's own arguments (start, E, P and table row, as passed)
-// come back through `req_args`, read once for the whole batch.  Returns
+// thread of the work-group takes part; `scratch` holds 7 * batch + 10 words
+// of LDS.  The request's own arguments (start, E, P and table row, as passed)
+// come back through `req_args`, read once for the whole batch.  The LDS loops
+// read four words per instruction so that their latencies overlap.  Returns
 // false when block k has no unit.
 __device__ bool ra_lpt_item(int32_t* scratch, int64_t k, int32_t hkv, int32_t batch, int32_t tpb,
                             const int32_t* __restrict__ req_pool_idx, const int32_t* __restrict__ prefix_lens,
                             const int32_t* __restrict__ extend_lens, const int32_t* __restrict__ extend_start,
                             int64_t total_tokens, int64_t rtt_stride, int& g, int& b, int& qt,
                             int32_t (&req_args)[4]) {
-  int32_t* args = scratch;              // [batch][4] start, E, P, table row as passed (16-byte entries)
-  int32_t* cost = scratch + 4 * batch;  // [batch] key count of the request's units, -1 if none
-  int32_t* nun = scratch + 5 * batch;   // [batch] units of the request; then units by rank
-  int32_t* ord = scratch + 6 * batch;   // [batch] request at each rank
-  int32_t* found = scratch + 7 * batch; // [2] request and unit offset of this block
+  const int bp = (batch + 3) & ~3;         // batch padded to whole int4 reads
+  int32_t* args = scratch;                 // [batch][4] start, E, P, table row as passed (16-byte entries)
+  int32_t* cost = scratch + 4 * batch;     // [bp] key count of the request's units, -1 if none, -2 padding
+  int32_t* nun = cost + bp;                // [batch] units of the request
+  int32_t* nrank = nun + batch;            // [bp] units by rank (0 padding)
+  int32_t* ord = nrank + bp;               // [batch] request at each rank
+  int32_t* found = ord + batch;            // [2] request and unit offset of this block
   const int tid = threadIdx.x, nt = blockDim.x;
   if (tid == 0) found[0] = -1;
-  for (int t = tid; t < batch; t += nt) {
+  for (int t = tid; t < bp; t += nt) {
+    if (t >= batch) {
+      cost[t] = -2;
+      nrank[t] = 0;
+      continue;
+    }
     const int32_t st = extend_start[t], el = extend_lens[t], pl = prefix_lens[t], rp = req_pool_idx[t];
     *reinterpret_cast<int4*>(&args[4 * t]) = make_int4(st, el, pl, rp);
     const int64_t e = (st < 0 || st > total_tokens) ? 0 : min<int64_t>(el, total_tokens - st);
@@ -113,6 +121,7 @@ __device__ bool ra_lpt_item(int32_t* scratch, int64_t k, int32_t hkv, int32_t ba
     cost[t] = nu > 0 ? static_cast<int32_t>(min<int64_t>(p + e, INT32_MAX)) : -1;
   }
   __syncthreads();
+  // rank = requests with a larger key count, or an equal one and a smaller index
   int32_t rk[4], nu_own[4];  // batch <= kLptMaxBatch <= 4 * blockDim.x
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
@@ -121,30 +130,45 @@ __device__ bool ra_lpt_item(int32_t* scratch, int64_t k, int32_t hkv, int32_t ba
     if (t < batch) {
       const int32_t c = cost[t];
       int rank = 0;
-      for (int s2 = 0; s2 < batch; ++s2) {
-        const int32_t cs = cost[s2];
-        rank += (cs > c) | ((cs == c) & (s2 < t));
+      for (int s4 = 0; s4 < bp; s4 += 4) {
+        const int4 cs = *reinterpret_cast<const int4*>(&cost[s4]);
+        rank += (cs.x > c) | ((cs.x == c) & (s4 < t));
+        rank += (cs.y > c) | ((cs.y == c) & (s4 + 1 < t));
+        rank += (cs.z > c) | ((cs.z == c) & (s4 + 2 < t));
+        rank += (cs.w > c) | ((cs.w == c) & (s4 + 3 < t));
       }
       rk[i] = rank;
       nu_own[i] = nun[t];
     }
   }
-  __syncthreads();
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     if (rk[i] >= 0) {
       ord[rk[i]] = tid + i * nt;
-      nun[rk[i]] = nu_own[i];  // nun now holds the unit counts in rank order
+      nrank[rk[i]] = nu_own[i];
     }
   }
   __syncthreads();
+  // Wave 0 scans the unit counts in rank order, 64 ranks at a time, and
+  // finds the rank whose units hold unit r.
   const int64_t r = k / hkv;
-  for (int j = tid; j < batch; j += nt) {
-    int64_t before = 0;
-    for (int i = 0; i < j; ++i) before += nun[i];
-    if (r >= before && r < before + nun[j]) {
-      found[0] = ord[j];
-      found[1] = static_cast<int32_t>(nun[j] - 1 - (r - before));
+  if (tid < 64) {
+    int64_t carry = 0;
+    for (int base = 0; base < batch; base += 64) {
+      const int j = base + tid;
+      const int32_t v = j < batch ? nrank[j] : 0;
+      int64_t incl = v;
+#pragma unroll
+      for (int d = 1; d < 64; d <<= 1) {
+        const int64_t up = __shfl_up(incl, d, 64);
+        if (tid >= d) incl += up;
+      }
+      const int64_t excl = carry + incl - v;
+      if (j < batch && r >= excl && r < excl + v) {
+        found[0] = ord[j];
+        found[1] = static_cast<int32_t>(v - 1 - (r - excl));
+      }
+      carry += __shfl(incl, 63, 64);
     }
   }
   __syncthreads();
@@ -813,7 +837,10 @@ static int extend_launch(const void* q, const void* k_new, const void* v_new, in
   auto* vp = static_cast<const __bf16*>(v_pool);
   auto* op = static_cast<__bf16*>(out);
   const int32_t nq = static_cast<int32_t>(n_qtiles);
-  const int32_t lpt = batch <= kLptMaxBatch ? 1 : 0;
+  // Longest first only matters when the work-groups take more than one round
+  // of the chip's work-group slots (two per CU with 128 rows, one with 256).
+  const int64_t slots = static_cast<int64_t>(ra_device_cus()) * (rows == 256 ? 1 : 2);
+  const int32_t lpt = batch <= kLptMaxBatch && items > slots ? 1 : 0;
 #define RA_WIDE_LAUNCH(DD, W, B)                                                                                   \
   launch_wide<DD, W, B>(items, stream, qp, knp, vnp, total_tokens, kp, vp, pool_slots, req_to_token, rtt_rows,     \
                         rtt_stride, req_pool_idx, prefix_lens, extend_lens, extend_start, batch, hkv, grp, nq, lpt, \
