@@ -138,6 +138,23 @@ def test_extend_work_order_batch_sizes(n_req):
     _check_all(run, inp, oe, od, f"order n_req={n_req}")
 
 
+@pytest.mark.parametrize("n_req", [700, 1600])
+def test_decode_large_batches(n_req):
+    """Large decode batches over two kv heads: several thousand (split,
+    request) items dealt to the XCDs in turn, ragged lengths with exact chunk
+    multiples, single tokens and equal lengths: every output against the
+    oracle."""
+    log(f"case: decode large batch n_req={n_req}")
+    rng = np.random.default_rng(5000 + n_req)
+    lens = [int(x) for x in rng.integers(1, 700, n_req)]
+    lens[1] = lens[2] = 256  # exact chunk multiples, equal lengths
+    lens[4] = 1
+    lens[6] = 1000
+    sc = _scenario(f"dorder{n_req}", 8, 2, 128, sum(lens) + 256, decode=lens, seed=23 + n_req)
+    run, inp, oe, od = _run(sc)
+    _check_all(run, inp, oe, od, f"decode order n_req={n_req}")
+
+
 @pytest.mark.parametrize("num_splits", [0, 1, 3, 16])
 def test_decode_boundaries(num_splits):
     lens = [1, 2, 31, 32, 33, 63, 64, 65, 255, 256, 257, 511, 512, 513, 1000, 2049]
