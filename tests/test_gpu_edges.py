@@ -119,11 +119,12 @@ def test_extend_kernels_agree_with_oracle(hq, hkv, d):
             assert_close(got[start:start + e], ref, f"{name} kernel P={p} E={e}")
 
 
-@pytest.mark.parametrize("n_req", [1024, 1100])
-def test_extend_work_order_batch_sizes(n_req):
+@pytest.mark.parametrize("n_req,hq,hkv", [(1024, 8, 2), (1100, 8, 2), (600, 16, 16)])
+def test_extend_work_order_batch_sizes(n_req, hq, hkv):
     """Up to 1024 requests the extend kernel starts its work items longest
     first (ranked inside each work-group); above that it keeps the static
-    order.  Both sides of the limit, with ragged and equal key counts (ties),
+    order.  Both sides of the limit, and 16 kv heads (two per XCD), with
+    ragged and equal key counts (ties),
     a request with no new tokens, and empty query-tile slots: every output
     row against the oracle."""
     log(f"case: extend work order n_req={n_req}")
@@ -133,7 +134,7 @@ def test_extend_work_order_batch_sizes(n_req):
     ext[7] = (30, 0)           # no new tokens
     ext[9] = (100, 40)         # longest, several query tiles of 128 rows / 4 heads
     pool = sum(p + e for p, e in ext) + 256
-    sc = _scenario(f"order{n_req}", 8, 2, 64, pool, extend=ext, seed=17 + n_req)
+    sc = _scenario(f"order{n_req}", hq, hkv, 64, pool, extend=ext, seed=17 + n_req)
     run, inp, oe, od = _run(sc)
     _check_all(run, inp, oe, od, f"order n_req={n_req}")
 
