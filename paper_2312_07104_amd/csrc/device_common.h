@@ -56,3 +56,7 @@ inline int ra_check_launch(const char* who) {
 }
 
 inline bool ra_aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// Compute units of the current device (cached per device; 256 if the query
+// fails).  Defined in extend.hip.
+int ra_device_cus();

@@ -804,7 +804,7 @@ void launch_wide(int64_t items, hipStream_t stream, const __bf16* qp, const __bf
 
 // Compute units of the current device (cached per device; 256 if the query
 // fails).
-static int ra_device_cus() {
+int ra_device_cus() {
   static std::atomic<int> cached[64] = {};
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;

@@ -156,6 +156,25 @@ def test_decode_large_batches(n_req):
     _check_all(run, inp, oe, od, f"decode order n_req={n_req}")
 
 
+def test_decode_longest_first():
+    """With 2048-token chunks and more items than the chip's wave slots, the
+    decode kernel starts the full chunks first and the partial last chunks
+    longest first.  Ragged lengths with exact chunk multiples, contexts
+    shorter than one chunk and equal lengths: every output against the
+    oracle."""
+    log("case: decode longest first")
+    rng = np.random.default_rng(6100)
+    lens = [int(x) for x in rng.integers(1, 4097, 128)]
+    lens[0] = lens[1] = 2048
+    lens[2] = 4096
+    lens[3] = lens[4] = 3000
+    lens[5] = 1
+    sc = _scenario("dlpt", 8, 8, 128, sum(lens) + 256, decode=lens, seed=61)
+    assert pa.ra_decode_chunk_len(len(lens), 8, max(lens), 2) == 2048
+    run, inp, oe, od = _run(sc, num_splits=2)
+    _check_all(run, inp, oe, od, "decode longest first")
+
+
 @pytest.mark.parametrize("num_splits", [0, 1, 3, 16])
 def test_decode_boundaries(num_splits):
     lens = [1, 2, 31, 32, 33, 63, 64, 65, 255, 256, 257, 511, 512, 513, 1000, 2049]
