@@ -4,7 +4,9 @@
 // long (evaluation, section 6.2); it is bound by HBM bandwidth, so the design
 // goal is a steady stream of gathered 256-byte K/V rows.
 //
-// Work item = (request, kv head, KV chunk); one wave per item.  Two
+// Work item = (request, kv head, KV chunk); one wave per item.  Items go out
+// in (split, request) order with the kv head fastest (ra_decode_item), or,
+// for chunks of 2048 tokens and up, longest first (ra_decode_lpt_item).  Two
 // partial-pass kernels share the item layout, the per-tile arithmetic and the
 // outputs: decode_partial_vr_kernel (D = 128) stages the gathered rows in
 // registers, decode_partial_kernel (D = 64) copies them straight into LDS:
