@@ -93,14 +93,18 @@ struct ra_cache {
   }
 
   // ---- pool ----
+  // (head and count stay in [0, pool_slots]: wrap by one comparison, no
+  // division per slot)
   void push_free(int32_t s) {
-    ring[(head + count) % pool_slots] = s;
+    int64_t at = head + count;
+    if (at >= pool_slots) at -= pool_slots;
+    ring[at] = s;
     ++count;
     is_free[s] = 1;
   }
   int32_t pop_free() {
     int32_t s = ring[head];
-    head = (head + 1) % pool_slots;
+    if (++head == pool_slots) head = 0;
     --count;
     is_free[s] = 0;
     return s;
@@ -255,23 +259,34 @@ int ra_alloc_slots(ra_cache* c, int64_t n, int32_t* out_slots) {
   return ra_guard("ra_alloc_slots", [&]() -> int {
     if (!c || n < 0 || (n > 0 && !out_slots)) return ra_fail(RA_EINVAL, "ra_alloc_slots: bad argument");
     if (n > c->count) return ra_fail(RA_ENOMEM, "ra_alloc_slots: not enough free slots");
-    for (int64_t i = 0; i < n; ++i) out_slots[i] = c->pop_free();
+    // the front n entries of the ring, in at most two runs
+    const int64_t first = std::min<int64_t>(n, c->pool_slots - c->head);
+    std::memcpy(out_slots, c->ring.data() + c->head, static_cast<size_t>(first) * sizeof(int32_t));
+    std::memcpy(out_slots + first, c->ring.data(), static_cast<size_t>(n - first) * sizeof(int32_t));
+    for (int64_t i = 0; i < n; ++i) c->is_free[out_slots[i]] = 0;
+    c->head += n;
+    if (c->head >= c->pool_slots) c->head -= c->pool_slots;
+    c->count -= n;
     return ra_ok();
   });
 }
 
 static int check_freeable(ra_cache* c, const int32_t* slots, int64_t n, const char* who) {
   // every slot in range, currently allocated, and not repeated
-  std::vector<int32_t> seen;
   for (int64_t i = 0; i < n; ++i) {
     int32_t s = slots[i];
     if (s < 0 || s >= c->pool_slots || c->is_free[s])
       return ra_fail(RA_EINVAL, std::string(who) + ": slot out of range or already free");
   }
-  seen.assign(slots, slots + n);
-  std::sort(seen.begin(), seen.end());
-  if (std::adjacent_find(seen.begin(), seen.end()) != seen.end())
-    return ra_fail(RA_EINVAL, std::string(who) + ": repeated slot");
+  // Repeats: mark each slot in the free map (all are allocated, so unmarked)
+  // and find a mark already set; the marks are cleared again either way.
+  int64_t i = 0;
+  for (; i < n; ++i) {
+    if (c->is_free[slots[i]]) break;
+    c->is_free[slots[i]] = 1;
+  }
+  for (int64_t j = 0; j < i; ++j) c->is_free[slots[j]] = 0;
+  if (i < n) return ra_fail(RA_EINVAL, std::string(who) + ": repeated slot");
   return RA_OK;
 }
 
