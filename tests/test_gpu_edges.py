@@ -156,20 +156,27 @@ def test_decode_large_batches(n_req):
     _check_all(run, inp, oe, od, f"decode order n_req={n_req}")
 
 
-def test_decode_longest_first():
+@pytest.mark.parametrize("kind", ["ragged", "full", "partial"])
+def test_decode_longest_first(kind):
     """With 2048-token chunks and more items than the chip's wave slots, the
     decode kernel starts the full chunks first and the partial last chunks
     longest first.  Ragged lengths with exact chunk multiples, contexts
-    shorter than one chunk and equal lengths: every output against the
-    oracle."""
-    log("case: decode longest first")
+    shorter than one chunk and equal lengths; batches of full chunks only
+    and of partial chunks only: every output against the oracle."""
+    log(f"case: decode longest first {kind}")
     rng = np.random.default_rng(6100)
-    lens = [int(x) for x in rng.integers(1, 4097, 128)]
-    lens[0] = lens[1] = 2048
-    lens[2] = 4096
-    lens[3] = lens[4] = 3000
-    lens[5] = 1
-    sc = _scenario("dlpt", 8, 8, 128, sum(lens) + 256, decode=lens, seed=61)
+    if kind == "full":
+        lens = [2048 * int(x) for x in rng.integers(1, 3, 128)]
+    elif kind == "partial":
+        lens = [int(x) for x in rng.integers(1, 2048, 128)]
+        lens[0] = 4096  # two full chunks, so num_splits = 2 keeps chunks 2048 long
+    else:
+        lens = [int(x) for x in rng.integers(1, 4097, 128)]
+        lens[0] = lens[1] = 2048
+        lens[2] = 4096
+        lens[3] = lens[4] = 3000
+        lens[5] = 1
+    sc = _scenario(f"dlpt_{kind}", 8, 8, 128, sum(lens) + 256, decode=lens, seed=61)
     assert pa.ra_decode_chunk_len(len(lens), 8, max(lens), 2) == 2048
     run, inp, oe, od = _run(sc, num_splits=2)
     _check_all(run, inp, oe, od, "decode longest first")
