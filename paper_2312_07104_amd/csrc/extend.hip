@@ -74,9 +74,11 @@ __device__ __forceinline__ void s_mfma_acc(f32x4_t& s, const bf16x8_t& a, const 
   asm("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0" : "+v"(s) : "v"(a), "a"(qa));
 }
 
-// Requests above this batch size keep the static item order (the ranking
-// below is quadratic in the batch and its scratch lives in the K/V ring).
-constexpr int kLptMaxBatch = 1024;  // 7 * 1024 + 10 words fit every configuration's ring
+// Requests above this batch size keep the static item order: the ranking
+// below is quadratic in the batch, and its scratch (8 * batch + 8 words)
+// lives in the K/V ring, whose smallest configuration (D = 64, 128 rows) has
+// 32 KB.
+constexpr int kLptMaxBatch = 1016;
 
 // Work item of block k in longest-first order.  A unit is (request, query
 // tile).  Units are ordered by their request's key count P + E, longest
@@ -87,7 +89,7 @@ constexpr int kLptMaxBatch = 1024;  // 7 * 1024 + 10 words fit every configurati
 // 8 | hkv each XCD keeps whole kv heads (its L2 sees their rows only).  A
 // static order would leave the longest items for the end when a batch fills
 // the chip only a few times over (short extends, head shards).  Every
-// thread of the work-group takes part; `scratch` holds 7 * batch + 10 words
+// thread of the work-group takes part; `scratch` holds 8 * batch + 8 words
 // of LDS.  The request's own arguments (start, E, P and table row, as passed)
 // come back through `req_args`, read once for the whole batch.  The LDS loops
 // read four words per instruction so that their latencies overlap.  Returns
@@ -212,6 +214,7 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void extend_kernel(
   constexpr int ROW_STEP = kBN / LOADS;       // a DMA lane covers rows u0 + it * ROW_STEP
   static_assert(LOADS == 1 || LOADS == 2, "index vector width");
   __shared__ __align__(16) unsigned char kv_lds[kStages * STAGE_B];
+  static_assert((8 * kLptMaxBatch + 8) * 4 <= kStages * STAGE_B, "ranking scratch exceeds the K/V ring");
   // one index copy moves 64 words (rows beyond the tile are never read)
   __shared__ __align__(16) int32_t idx_lds[kRing][64];
 

@@ -119,9 +119,9 @@ def test_extend_kernels_agree_with_oracle(hq, hkv, d):
             assert_close(got[start:start + e], ref, f"{name} kernel P={p} E={e}")
 
 
-@pytest.mark.parametrize("n_req,hq,hkv", [(1024, 8, 2), (1100, 8, 2), (600, 16, 16)])
+@pytest.mark.parametrize("n_req,hq,hkv", [(1016, 8, 2), (1100, 8, 2), (600, 16, 16)])
 def test_extend_work_order_batch_sizes(n_req, hq, hkv):
-    """Up to 1024 requests the extend kernel starts its work items longest
+    """Up to 1016 requests the extend kernel starts its work items longest
     first (ranked inside each work-group); above that it keeps the static
     order.  Both sides of the limit, and 16 kv heads (two per XCD), with
     ragged and equal key counts (ties),
