@@ -156,14 +156,15 @@ def test_decode_large_batches(n_req):
     _check_all(run, inp, oe, od, f"decode order n_req={n_req}")
 
 
-@pytest.mark.parametrize("kind", ["ragged", "full", "partial"])
-def test_decode_longest_first(kind):
+@pytest.mark.parametrize("kind,d", [("ragged", 128), ("full", 128), ("partial", 128), ("ragged", 64)])
+def test_decode_longest_first(kind, d):
     """With 2048-token chunks and more items than the chip's wave slots, the
     decode kernel starts the full chunks first and the partial last chunks
     longest first.  Ragged lengths with exact chunk multiples, contexts
     shorter than one chunk and equal lengths; batches of full chunks only
-    and of partial chunks only: every output against the oracle."""
-    log(f"case: decode longest first {kind}")
+    and of partial chunks only; both partial-pass kernels (D = 128 register
+    staging, D = 64 LDS copies): every output against the oracle."""
+    log(f"case: decode longest first {kind} d={d}")
     rng = np.random.default_rng(6100)
     if kind == "full":
         lens = [2048 * int(x) for x in rng.integers(1, 3, 128)]
@@ -176,7 +177,7 @@ def test_decode_longest_first(kind):
         lens[2] = 4096
         lens[3] = lens[4] = 3000
         lens[5] = 1
-    sc = _scenario(f"dlpt_{kind}", 8, 8, 128, sum(lens) + 256, decode=lens, seed=61)
+    sc = _scenario(f"dlpt_{kind}_{d}", 8, 8, d, sum(lens) + 256, decode=lens, seed=61)
     assert pa.ra_decode_chunk_len(len(lens), 8, max(lens), 2) == 2048
     run, inp, oe, od = _run(sc, num_splits=2)
     _check_all(run, inp, oe, od, "decode longest first")
