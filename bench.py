@@ -215,7 +215,7 @@ def main():
     import torch
 
     import paper_2312_07104_amd as pa
-    from tests.harness import ScenarioRun
+    from workload.driver import ScenarioRun
     from workload import scenarios as S
 
     sc = S.ALL[args.workload]()

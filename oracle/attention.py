@@ -23,6 +23,8 @@ printed number.
 """
 from __future__ import annotations
 
+import time
+
 import numpy as np
 
 from workload import contentgen as cg
@@ -61,30 +63,59 @@ def attend(q: np.ndarray, k: np.ndarray, v: np.ndarray, q_pos: np.ndarray, scale
     return out
 
 
-def request_kv(tokens: np.ndarray, seed: int, hkv: int, d: int, upto: int | None = None):
-    """Regenerate a request's K and V [L, Hkv, D] from its own token list."""
+def request_kv(tokens: np.ndarray, seed: int, hkv: int, d: int, upto: int | None = None,
+               key_patches: dict | None = None):
+    """Regenerate a request's K and V [L, Hkv, D] from its own token list.
+
+    ``key_patches`` overrides inputs: {prefix hash: {kv head: K row [D]}}.  A
+    position whose prefix hash is listed takes that K row for that kv head
+    (a test plants such keys in the pool, so every request whose context
+    holds the same prefix sees the same key, as the pool would serve it).
+    """
     t = np.asarray(tokens)[: len(tokens) if upto is None else upto]
     h = cg.prefix_hashes(t, seed)
-    return cg.values(h, cg.STREAM_K, hkv, d), cg.values(h, cg.STREAM_V, hkv, d), h
+    k = cg.values(h, cg.STREAM_K, hkv, d)
+    if key_patches:
+        for p in np.flatnonzero(np.isin(h, np.fromiter(key_patches.keys(), dtype=np.uint64))):
+            for g, row in key_patches[int(h[p])].items():
+                k[p, g] = row
+    return k, cg.values(h, cg.STREAM_V, hkv, d), h
 
 
 def extend_reference(tokens: np.ndarray, prefix_len: int, extend_len: int, seed: int,
                      hq: int, hkv: int, d: int, scale: float, q_scale_pow2: int = 0,
-                     rows: np.ndarray | None = None) -> np.ndarray:
+                     rows: np.ndarray | None = None, key_patches: dict | None = None,
+                     timings: dict | None = None) -> np.ndarray:
     """Output rows of an extend request, float64 [len(rows) or E, Hq, D].
 
     ``rows`` selects new-token indices (0 .. E-1) to compute; default all.
+    ``key_patches`` as in ``request_kv``.  ``timings``, when given, gets the
+    seconds spent regenerating inputs ("regen") and attending ("attend").
     """
+    t0 = time.perf_counter()
     n = prefix_len + extend_len
-    k, v, h = request_kv(tokens, seed, hkv, d, upto=n)
+    k, v, h = request_kv(tokens, seed, hkv, d, upto=n, key_patches=key_patches)
     rows = np.arange(extend_len) if rows is None else np.asarray(rows, dtype=np.int64)
     q = cg.values(h[prefix_len + rows], cg.STREAM_Q, hq, d, q_scale_pow2)
-    return attend(q, k, v, prefix_len + rows, scale)
+    t1 = time.perf_counter()
+    out = attend(q, k, v, prefix_len + rows, scale)
+    if timings is not None:
+        timings["regen"] = timings.get("regen", 0.0) + t1 - t0
+        timings["attend"] = timings.get("attend", 0.0) + time.perf_counter() - t1
+    return out
 
 
 def decode_reference(tokens: np.ndarray, seq_len: int, seed: int, hq: int, hkv: int, d: int,
-                     scale: float, q_scale_pow2: int = 0) -> np.ndarray:
-    """Output of a decode request (query at position L-1), float64 [Hq, D]."""
-    k, v, h = request_kv(tokens, seed, hkv, d, upto=seq_len)
+                     scale: float, q_scale_pow2: int = 0, key_patches: dict | None = None,
+                     timings: dict | None = None) -> np.ndarray:
+    """Output of a decode request (query at position L-1), float64 [Hq, D].
+    ``key_patches`` and ``timings`` as in ``extend_reference``."""
+    t0 = time.perf_counter()
+    k, v, h = request_kv(tokens, seed, hkv, d, upto=seq_len, key_patches=key_patches)
     q = cg.values(h[seq_len - 1 : seq_len], cg.STREAM_Q, hq, d, q_scale_pow2)
-    return attend(q, k, v, np.array([seq_len - 1]), scale)[0]
+    t1 = time.perf_counter()
+    out = attend(q, k, v, np.array([seq_len - 1]), scale)[0]
+    if timings is not None:
+        timings["regen"] = timings.get("regen", 0.0) + t1 - t0
+        timings["attend"] = timings.get("attend", 0.0) + time.perf_counter() - t1
+    return out

@@ -1,199 +1,189 @@
-"""Drives a seeded workload through the GPU path (tests, smoke and bench).
+"""GPU-side helpers of the parity tests: needle planting, the table -> pool
+content check and oracle comparisons over a process pool.
 
-The host side uses the package's Scheduler (native radix cache) to build slot
-tables; the KV pool's cached positions are filled by the GPU value generator
-from each position's prefix hash; new tokens' Q/K/V come from the same
-generator and are stored with ``ra_store_kv``.  Nothing here computes
-attention: outputs come from the package's kernels, expected values from the
-oracle (imported by the tests, not here).
+The workload driver (``workload.driver``) builds the inputs and calls the
+package's kernels; expected values come from the oracle.  Nothing here
+computes attention.  Tolerances and needle arithmetic live in ``tests.gate``.
 """
 from __future__ import annotations
 
-import sys
-import time
 from dataclasses import dataclass
 
 import numpy as np
 import torch
 
-import paper_2312_07104_amd as pa
-from paper_2312_07104_amd.runtime import BatchPlan, Scheduler, build_table
+from oracle import pool as opool
+from tests.gate import MAX_ABS, MEAN_ABS, REL_RMS, assert_close, errors, needle_key  # noqa: F401
 from workload import contentgen as cg
 from workload import gpu_gen
+from workload.driver import PhaseInputs, ScenarioRun, log  # noqa: F401  (re-exported for the tests)
 
 
-def log(*a):
-    print(*a, file=sys.stderr, flush=True)
+def make_scenario(name, hq, hkv, d, pool, extend=(), decode=(), seed=77, q_pow2=0):
+    """A one-batch scenario of private token runs: extend requests (P, E) and
+    decode requests of context L, no history."""
+    from workload import scenarios as S
+
+    ext = [S.ExtendReq(cg.run_tokens(seed * 1000 + i, p + e, S.VOCAB), p, e) for i, (p, e) in enumerate(extend)]
+    dec = [S.DecodeReq(cg.run_tokens(seed * 1000 + 500 + i, l, S.VOCAB), l) for i, l in enumerate(decode)]
+    sc = S.Scenario(name, seed, hq, hkv, d, pool, 0, lambda i: None, [S.Phase(extend=ext, decode=dec)])
+    sc.q_scale_pow2 = q_pow2
+    return sc
 
 
 @dataclass
-class PhaseInputs:
-    plan: BatchPlan
-    n_ext: int
-    n_dec: int
-    hashes: list            # per request, uint64 prefix hashes of its sequence
-    table: torch.Tensor     # req_to_token [R, stride] int32
-    rpi: torch.Tensor       # req_pool_idx [R] int32 (extends first, then decodes)
-    prefix_lens: torch.Tensor
-    extend_lens: torch.Tensor
-    extend_start: torch.Tensor
-    seq_lens: torch.Tensor
-    max_extend_len: int
-    max_seq_len: int
-    total_ext: int
-    q_ext: torch.Tensor      # [sum E, Hq, D]
-    q_dec: torch.Tensor      # [B_dec, Hq, D]
-    k_new: torch.Tensor      # [sum E + B_dec, Hkv, D]
-    v_new: torch.Tensor
-    new_slots: torch.Tensor  # [sum E + B_dec] int32
-    ext_meta: list           # (tokens, P, E, start row)
-    dec_meta: list           # (tokens, L)
+class Needle:
+    """A planted key: request ``req`` of kind "ext" (query = new token ``row``,
+    position P + row) or "dec" (query at L - 1); query head ``head``; key
+    position ``pos`` (<= the query's position)."""
+    kind: str
+    req: int
+    head: int
+    pos: int
+    row: int = 0
+    share: float = 0.5
 
 
-class ScenarioRun:
-    def __init__(self, sc, device: str = "cuda", history_limit: int | None = None, row_perm_seed: int = 7,
-                 pool=None):
-        self.sc = sc
-        self.device = device
-        self.sched = Scheduler(sc.pool_slots, sc.free_order())
-        n_hist = sc.history_len if history_limit is None else min(history_limit, sc.history_len)
-        t0 = time.perf_counter()
-        for i in range(n_hist):
-            self.sched.finish_request(sc.history(i))
-        self.history_seconds = time.perf_counter() - t0
-        self.history_ops = self.sched.ops
-        self.row_perm_seed = row_perm_seed
-        if pool is None:
-            shape = (sc.pool_slots, sc.hkv, sc.d)
-            self.k_pool = torch.empty(shape, dtype=torch.bfloat16, device=device)
-            self.v_pool = torch.empty(shape, dtype=torch.bfloat16, device=device)
-        else:
-            self.k_pool, self.v_pool = pool
-        self.filled = np.zeros(sc.pool_slots, dtype=bool)
-
-    # -- inputs --------------------------------------------------------------
-    def prepare(self, idx: int) -> PhaseInputs:
-        sc, dev = self.sc, self.device
-        ph = sc.phases[idx]
-        ext = [(r.tokens, r.prefix_len, r.extend_len) for r in ph.extend]
-        dec = [(r.tokens, r.seq_len) for r in ph.decode]
-        t0 = time.perf_counter()
-        plan = self.sched.plan_batch(ext, dec)
-        self.plan_seconds = time.perf_counter() - t0
-        seqs = [np.asarray(t)[: p + e] for t, p, e in ext] + [np.asarray(t)[:l] for t, l in dec]
-        hashes = [cg.prefix_hashes(s, sc.seed) for s in seqs]
-
-        # cached context positions not yet holding their values
-        fs, fh = [], []
-        for row, h, c in zip(plan.rows, hashes, plan.ctx_lens):
-            s = row[:c]
-            need = ~self.filled[s]
-            fs.append(s[need])
-            fh.append(h[:c][need])
-        if fs:
-            s_all = np.concatenate(fs)
-            h_all = np.concatenate(fh)
-            s_u, first = np.unique(s_all, return_index=True)
-            if s_u.size:
-                gpu_gen.fill(self.k_pool, h_all[first], cg.STREAM_K, rows=s_u)
-                gpu_gen.fill(self.v_pool, h_all[first], cg.STREAM_V, rows=s_u)
-                self.filled[s_u] = True
-
-        n_ext, n_dec = len(ext), len(dec)
-        ext_h = [hashes[i][p: p + e] for i, (t, p, e) in enumerate(ext)]
-        dec_h = [hashes[n_ext + i][l - 1: l] for i, (t, l) in enumerate(dec)]
-        qh_ext = np.concatenate(ext_h) if ext_h else np.zeros(0, np.uint64)
-        qh_dec = np.concatenate(dec_h) if dec_h else np.zeros(0, np.uint64)
-        new_h = np.concatenate([qh_ext, qh_dec])
-        total_ext = int(qh_ext.shape[0])
-        hq, hkv, d = sc.hq, sc.hkv, sc.d
-        q_ext = torch.empty((max(total_ext, 1), hq, d), dtype=torch.bfloat16, device=dev)[:total_ext]
-        q_dec = torch.empty((max(n_dec, 1), hq, d), dtype=torch.bfloat16, device=dev)[:n_dec]
-        k_new = torch.empty((max(new_h.shape[0], 1), hkv, d), dtype=torch.bfloat16, device=dev)[: new_h.shape[0]]
-        v_new = torch.empty_like(k_new)
-        if total_ext:
-            gpu_gen.fill(q_ext, qh_ext, cg.STREAM_Q, scale_pow2=sc.q_scale_pow2)
-        if n_dec:
-            gpu_gen.fill(q_dec, qh_dec, cg.STREAM_Q, scale_pow2=sc.q_scale_pow2)
-        if new_h.shape[0]:
-            gpu_gen.fill(k_new, new_h, cg.STREAM_K)
-            gpu_gen.fill(v_new, new_h, cg.STREAM_V)
-        new_slots = np.concatenate(
-            [plan.rows[i][p: p + e] for i, (t, p, e) in enumerate(ext)]
-            + [plan.rows[n_ext + i][l - 1: l] for i, (t, l) in enumerate(dec)]
-        ).astype(np.int32) if (ext or dec) else np.zeros(0, np.int32)
-
-        rng = np.random.default_rng(self.row_perm_seed)
-        order = rng.permutation(n_ext + n_dec).astype(np.int32)
-        table, rpi = build_table(plan.rows, row_order=order)
-        starts = np.cumsum([0] + [e for _, _, e in ext])[:-1] if ext else np.zeros(0, np.int64)
-        ext_meta = [(t, p, e, int(s)) for (t, p, e), s in zip(ext, starts)]
-
-        def dt(a):
-            return torch.from_numpy(np.ascontiguousarray(a, dtype=np.int32)).to(dev)
-
-        return PhaseInputs(
-            plan=plan, n_ext=n_ext, n_dec=n_dec, hashes=hashes, table=dt(table), rpi=dt(rpi),
-            prefix_lens=dt([p for _, p, _ in ext]), extend_lens=dt([e for _, _, e in ext]),
-            extend_start=dt(starts), seq_lens=dt([l for _, l in dec]),
-            max_extend_len=max([e for _, _, e in ext], default=0), max_seq_len=max([l for _, l in dec], default=0),
-            total_ext=total_ext, q_ext=q_ext, q_dec=q_dec, k_new=k_new, v_new=v_new,
-            new_slots=dt(new_slots), ext_meta=ext_meta, dec_meta=dec)
-
-    # -- the hot path ----------------------------------------------------------
-    def store(self, inp: PhaseInputs) -> None:
-        if inp.new_slots.shape[0]:
-            pa.ra_store_kv(inp.new_slots, inp.k_new, inp.v_new, self.k_pool, self.v_pool)
-            self.filled[inp.new_slots.cpu().numpy()] = True
-
-    def extend(self, inp: PhaseInputs, out=None):
-        if inp.n_ext == 0:
-            return None
-        return pa.ra_extend_attention(
-            inp.q_ext, inp.k_new[: inp.total_ext], inp.v_new[: inp.total_ext], self.k_pool, self.v_pool,
-            inp.table, inp.rpi[: inp.n_ext], inp.prefix_lens, inp.extend_lens, inp.extend_start,
-            inp.max_extend_len, self.sc.scale, out=out)
-
-    def decode(self, inp: PhaseInputs, num_splits: int = 0, workspace=None, out=None):
-        if inp.n_dec == 0:
-            return None
-        return pa.ra_decode_attention(
-            inp.q_dec, self.k_pool, self.v_pool, inp.table, inp.rpi[inp.n_ext:], inp.seq_lens, inp.max_seq_len,
-            self.sc.scale, num_splits=num_splits, workspace=workspace, out=out)
-
-    def mixed(self, inp: PhaseInputs, num_splits: int = 0, workspace=None, out_ext=None, out_dec=None):
-        """Both halves of the batch in one ra_mixed_attention call."""
-        if inp.n_ext == 0 or inp.n_dec == 0:
-            return self.extend(inp, out=out_ext), self.decode(inp, num_splits, workspace, out_dec)
-        return pa.ra_mixed_attention(
-            inp.q_ext, inp.k_new[: inp.total_ext], inp.v_new[: inp.total_ext], inp.rpi[: inp.n_ext],
-            inp.prefix_lens, inp.extend_lens, inp.extend_start, inp.max_extend_len, inp.q_dec,
-            inp.rpi[inp.n_ext:], inp.seq_lens, inp.max_seq_len, self.k_pool, self.v_pool, inp.table, self.sc.scale,
-            num_splits=num_splits, workspace=workspace, out_ext=out_ext, out_dec=out_dec)
-
-    def finish(self, idx: int, inp: PhaseInputs) -> None:
-        ph = self.sc.phases[idx]
-        ext = [(r.tokens, r.prefix_len, r.extend_len) for r in ph.extend]
-        dec = [(r.tokens, r.seq_len) for r in ph.decode]
-        self.sched.finish_batch(ext, dec, inp.plan)
+def _req_view(inp: PhaseInputs, kind: str, req: int):
+    """(batch index, hashes, query position, extend start row or None)."""
+    if kind == "ext":
+        toks, p, e, start = inp.ext_meta[req]
+        return req, inp.hashes[req], p, start
+    toks, l = inp.dec_meta[req]
+    return inp.n_ext + req, inp.hashes[inp.n_ext + req], l - 1, None
 
 
-def errors(got: np.ndarray, ref: np.ndarray) -> dict:
-    got = np.asarray(got, dtype=np.float64)
-    ref = np.asarray(ref, dtype=np.float64)
-    e = np.abs(got - ref)
-    return {"max": float(e.max()) if e.size else 0.0, "mean": float(e.mean()) if e.size else 0.0,
-            "rel_rms": float(np.sqrt((e ** 2).sum() / max((ref ** 2).sum(), 1e-300)))}
+def plant_needles(run: ScenarioRun, inp: PhaseInputs, needles: list[Needle], prior: dict | None = None) -> dict:
+    """Writes needle keys into the GPU inputs after ``run.store(inp)``.
+
+    Each needle's key row is computed on the host (``needle_key`` against the
+    target query's other keys, regenerated from the content generator) and
+    written for its kv head at every (request, position) of the batch that
+    holds the same prefix hash: the pool slot from the plan, and for an
+    extend's new positions also the k_new row the extend kernel reads.
+    Returns the oracle's ``key_patches`` ({prefix hash: {kv head: row}}),
+    including ``prior`` patches (needles an earlier batch left in the pool).
+    """
+    sc = run.sc
+    grp = sc.hq // sc.hkv
+    patches: dict = {hh: dict(rows) for hh, rows in (prior or {}).items()}
+    touched: set = set()
+    kcache: dict = {}
+    for nd in needles:
+        bi, h, p0, _ = _req_view(inp, nd.kind, nd.req)
+        qpos = p0 + (nd.row if nd.kind == "ext" else 0)
+        assert 0 <= nd.pos <= qpos, (nd, qpos)
+        g = nd.head // grp
+        if bi not in kcache:
+            kcache[bi] = cg.values(h, cg.STREAM_K, sc.hkv, sc.d)
+        q = cg.values(h[qpos:qpos + 1], cg.STREAM_Q, sc.hq, sc.d, sc.q_scale_pow2)[0, nd.head]
+        k = kcache[bi][:qpos + 1, g].copy()
+        for hh, rows in patches.items():  # needles planted earlier in this context
+            if g in rows:
+                k[h[:qpos + 1] == np.uint64(hh)] = rows[g]
+        others = np.delete(k, nd.pos, axis=0)
+        patches.setdefault(int(h[nd.pos]), {})[g] = needle_key(q, others, sc.scale, nd.share)
+        touched.add(int(h[nd.pos]))
+    if not touched:
+        return patches
+    # every (request, position) of the batch holding a patched hash
+    new = {hh: patches[hh] for hh in touched}
+    keys = np.fromiter(new.keys(), dtype=np.uint64)
+    kp = run.k_pool
+    for bi, (h, row) in enumerate(zip(inp.hashes, inp.plan.rows)):
+        hits = np.flatnonzero(np.isin(h, keys))  # the plan's row holds every position of the context
+        for p in hits:
+            for g, krow in new[int(h[p])].items():
+                t = torch.from_numpy(krow).to(device=kp.device, dtype=torch.bfloat16)
+                kp[int(row[p]), g] = t
+                if bi < inp.n_ext:
+                    _, pfx, _, start = inp.ext_meta[bi]
+                    if p >= pfx:
+                        inp.k_new[start + (p - pfx), g] = t
+    torch.cuda.synchronize()
+    return patches
 
 
-# Tolerances: the spec bar for bf16 output against the float64 oracle,
-# plus a relative-RMS bound that a dropped or duplicated key would break.
-MAX_ABS = 2e-2
-MEAN_ABS = 2e-3
-REL_RMS = 1e-2
+def check_table_pool(run: ScenarioRun, inp: PhaseInputs, cpu_sample: int = 20000, seed: int = 0,
+                     key_patches: dict | None = None) -> dict:
+    """Table -> pool content check (bit for bit) for every attended position.
+
+    * the device table row req_pool_idx[r] equals the plan's slot row of
+      request r over its context;
+    * no slot is reachable from two different prefix hashes;
+    * pool[slot] holds the generator's K and V of that position's hash
+      (against the GPU generator for every position, and against the CPU
+      generator on a random sample); a position whose hash carries a needle
+      (``key_patches``) must hold the needle's K row instead.
+    """
+    sc = run.sc
+    table = inp.table.cpu().numpy()
+    rpi = inp.rpi.cpu().numpy()
+    slots_all, hashes_all = [], []
+    for bi, (h, row) in enumerate(zip(inp.hashes, inp.plan.rows)):
+        n = len(h)
+        got = table[rpi[bi], :n]
+        assert np.array_equal(got, np.asarray(row[:n], dtype=np.int32)), f"table row of request {bi}"
+        slots_all.append(got.astype(np.int64))
+        hashes_all.append(h)
+    slots = np.concatenate(slots_all)
+    hashes = np.concatenate(hashes_all)
+    order = np.argsort(slots, kind="stable")
+    s_sorted, h_sorted = slots[order], hashes[order]
+    same_slot = s_sorted[1:] == s_sorted[:-1]
+    assert not np.any(same_slot & (h_sorted[1:] != h_sorted[:-1])), "a slot is reachable from two prefix hashes"
+    first = np.concatenate([[True], ~same_slot])
+    u_slots, u_hashes = s_sorted[first], h_sorted[first]
+    patch_keys = np.fromiter((key_patches or {}).keys(), dtype=np.uint64)
+    chunk = 1 << 17
+    for a in range(0, u_slots.shape[0], chunk):
+        s_t = torch.from_numpy(u_slots[a:a + chunk]).to(run.k_pool.device)
+        for pool, stream in ((run.k_pool, cg.STREAM_K), (run.v_pool, cg.STREAM_V)):
+            exp = torch.empty((s_t.shape[0],) + tuple(pool.shape[1:]), dtype=torch.bfloat16, device=pool.device)
+            gpu_gen.fill(exp, u_hashes[a:a + chunk], stream)
+            if key_patches and stream == cg.STREAM_K:
+                for i in np.flatnonzero(np.isin(u_hashes[a:a + chunk], patch_keys)):
+                    for g, krow in key_patches[int(u_hashes[a + i])].items():
+                        exp[int(i), g] = torch.from_numpy(krow).to(device=pool.device, dtype=torch.bfloat16)
+            assert torch.equal(pool[s_t], exp), f"pool content differs from the generator (slots {a}..)"
+    rng = np.random.default_rng(seed)
+    plain = np.flatnonzero(~np.isin(u_hashes, patch_keys))
+    pick = plain[rng.choice(plain.shape[0], min(cpu_sample, plain.shape[0]), replace=False)]
+    s_t = torch.from_numpy(u_slots[pick]).to(run.k_pool.device)
+    for pool, stream in ((run.k_pool, cg.STREAM_K), (run.v_pool, cg.STREAM_V)):
+        got = pool[s_t].view(torch.int16).cpu().numpy().view(np.uint16).reshape(len(pick), -1)
+        assert np.array_equal(got, cg.values_bf16_bits(u_hashes[pick], stream, sc.hkv * sc.d)), "CPU sample"
+    return {"positions": int(slots.shape[0]), "distinct_slots": int(u_slots.shape[0])}
 
 
-def assert_close(got, ref, what: str = "") -> dict:
-    er = errors(got, ref)
-    assert er["max"] <= MAX_ABS and er["mean"] <= MEAN_ABS and er["rel_rms"] <= REL_RMS, f"{what}: {er}"
-    return er
+def oracle_check(run: ScenarioRun, inp: PhaseInputs, out_ext=None, out_dec=None, ext_rows=None, dec_reqs=None,
+                 key_patches=None, what: str = "", workers: int | None = None) -> dict:
+    """Compares kernel outputs with the oracle, requests spread over a
+    process pool.  ``ext_rows``: {extend request: new-token rows} (default:
+    none); ``dec_reqs``: decode requests to check (default: none).  Returns
+    the worst errors per kind."""
+    sc = run.sc
+    tasks, keys = [], []
+    for r, rows in (ext_rows or {}).items():
+        toks, p, e, start = inp.ext_meta[r]
+        rows = np.asarray(sorted(set(int(x) for x in rows)), dtype=np.int64)
+        tasks.append(opool.extend_task(toks, p, e, sc.seed, sc.hq, sc.hkv, sc.d, sc.scale, sc.q_scale_pow2, rows,
+                                       key_patches))
+        keys.append(("ext", r, start + rows))
+    for r in dec_reqs or []:
+        toks, l = inp.dec_meta[r]
+        tasks.append(opool.decode_task(toks, l, sc.seed, sc.hq, sc.hkv, sc.d, sc.scale, sc.q_scale_pow2,
+                                       key_patches))
+        keys.append(("dec", r, None))
+    got_e = None if out_ext is None else out_ext.float().cpu().numpy()
+    got_d = None if out_dec is None else out_dec.float().cpu().numpy()
+    worst = {}
+    with opool.OraclePool(workers) as pool:
+        for i, ref, _ in pool.imap(tasks):
+            kind, r, rows = keys[i]
+            got = got_e[rows] if kind == "ext" else got_d[r]
+            er = assert_close(got, ref, f"{what} {kind} request {r}")
+            if kind not in worst or er["max"] > worst[kind]["max"]:
+                worst[kind] = dict(er, req=r)
+    log(f"{what}: checked {len(tasks)} requests, worst {worst}")
+    return worst

@@ -17,7 +17,9 @@ pytestmark = pytest.mark.gpu
 if not torch.cuda.is_available():  # pragma: no cover - CPU-only container
     pytest.skip("no GPU", allow_module_level=True)
 
-from tests.harness import ScenarioRun, assert_close, errors, log  # noqa: E402
+import paper_2312_07104_amd as pa  # noqa: E402
+from tests.harness import (Needle, ScenarioRun, assert_close, check_table_pool, errors, log,  # noqa: E402
+                           oracle_check, plant_needles)
 
 
 def _bf(t):
@@ -175,11 +177,17 @@ def test_branching_two_phases():
     log("branching decode worst", er)
 
 
-def test_mixed_full_size_sampled():
-    """The headline batch through the one mixed call (extend and decode on
-    two streams): both outputs equal separate calls bit for bit, and sampled
-    rows match the oracle."""
+def test_mixed_full_size():
+    """The headline batch (64 / 8 / 128 heads, 32 extends and 512 decodes over
+    a 4,194,304-slot pool) through the one mixed call, as bench.py launches
+    it.  The table -> pool content check covers every attended position; the
+    mixed call equals separate calls bit for bit; then needles go to the
+    decode chunk edges (4096-token chunks, longest-first order), the first
+    and last positions, and to the extends' last cached key, first new key,
+    causal diagonal and tile edges.  Every decode request and every extend
+    request (needle rows plus a sample of others) against the oracle."""
     sc = S.cfg5_mixed()
+    grp = sc.hq // sc.hkv
     log(f"case: mixed seed={sc.seed} (history replay on host)")
     run = ScenarioRun(sc)
     log(f"history ops={run.history_ops} in {run.history_seconds:.2f}s")
@@ -187,12 +195,33 @@ def test_mixed_full_size_sampled():
     oe, od = run.mixed(inp)
     torch.cuda.synchronize()
     assert torch.equal(oe, oe_sep) and torch.equal(od, od_sep)
-    er = check_extend(run, inp, oe, sample=[0, 13, 31], rows_per_req=16, what="mixed/extend")
-    log("mixed extend worst", er)
-    lens = np.array([l for _, l in inp.dec_meta])
-    er = check_decode(run, inp, od, sample=sorted({int(lens.argmax()), int(lens.argmin()), 5, 300}),
-                      what="mixed/decode")
-    log("mixed decode worst", er)
+    log("table -> pool", check_table_pool(run, inp))
+    chunk = pa.ra_decode_chunk_len(inp.n_dec, sc.hkv, inp.max_seq_len, 0)
+    assert chunk == 4096
+    needles = []
+    lens = [l for _, l in inp.dec_meta]
+    long_reqs = [r for r, l in enumerate(lens) if l > 3 * chunk][:24]
+    for r in long_reqs:
+        L = lens[r]
+        cands = [0, 31, 32, chunk - 1, chunk, 2 * chunk - 1, 2 * chunk, 3 * chunk - 1, 3 * chunk, L - 2, L - 1]
+        for g in range(sc.hkv):
+            needles.append(Needle("dec", r, g * grp + (r + g) % grp, cands[(r + 3 * g) % len(cands)]))
+    rng = np.random.default_rng(55)
+    ext_rows = {}
+    for r, (toks, P, E, start) in enumerate(inp.ext_meta):
+        want = [(0, P - 1), (0, P), (E - 1, 0), (63, P + 63), (64, P + 64), (64, P + 63), (E - 1, P + E - 1),
+                (E - 1, 64), (E - 1, P + 64)]
+        for k, (i, pos) in enumerate(want):
+            if (r + k) % 3 == 0 and i < E and pos <= P + i:
+                needles.append(Needle("ext", r, (5 * r + 11 * k) % sc.hq, pos, row=i))
+        ext_rows[r] = sorted({0, 63, 64, E - 1} | {i for i, _ in want if i < E} |
+                             set(int(x) for x in rng.choice(E, 6, replace=False)))
+    log(f"planting {len(needles)} needles")
+    patches = plant_needles(run, inp, needles)
+    oe, od = run.mixed(inp)
+    torch.cuda.synchronize()
+    oracle_check(run, inp, out_ext=oe, out_dec=od, ext_rows=ext_rows, dec_reqs=range(inp.n_dec),
+                 key_patches=patches, what="mixed full size")
 
 
 def test_mixed_small_full():

@@ -15,23 +15,12 @@ if not torch.cuda.is_available():  # pragma: no cover
 
 import paper_2312_07104_amd as pa  # noqa: E402
 from tests.harness import ScenarioRun, assert_close, log  # noqa: E402
+from tests.harness import make_scenario as _scenario  # noqa: E402
 from workload import gpu_gen  # noqa: E402
 
 
 def _bf(t):
     return t.float().cpu().numpy()
-
-
-def _scenario(name, hq, hkv, d, pool, extend=(), decode=(), seed=77, q_pow2=0):
-    ext = []
-    for i, (p, e) in enumerate(extend):
-        ext.append(S.ExtendReq(cg.run_tokens(seed * 1000 + i, p + e, S.VOCAB), p, e))
-    dec = []
-    for i, l in enumerate(decode):
-        dec.append(S.DecodeReq(cg.run_tokens(seed * 1000 + 500 + i, l, S.VOCAB), l))
-    sc = S.Scenario(name, seed, hq, hkv, d, pool, 0, lambda i: None, [S.Phase(extend=ext, decode=dec)])
-    sc.q_scale_pow2 = q_pow2
-    return sc
 
 
 def _run(sc, num_splits=0):
