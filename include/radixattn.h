@@ -212,6 +212,26 @@ int ra_decode_attention(const void* q, const void* k_pool, const void* v_pool, i
 /* The chunk length (tokens) decode uses for these arguments. */
 int32_t ra_decode_chunk_len(int32_t batch, int32_t hkv, int32_t max_seq_len, int32_t num_splits);
 
+/* Decode attention that allocates nothing, for callers that cannot allocate
+ * device memory or pass a workspace (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid allocation).  Same arguments, results
+ * and rules as ra_decode_attention without the workspace: the split partials
+ * live in a library-owned device array of ra_decode_noalloc_max_scratch_bytes()
+ * bytes (128 MiB) per device, set up on the first call that needs it on a
+ * device and held until the process ends.  A batch whose
+ * ra_decode_workspace_bytes(...) exceeds that maximum is rejected with
+ * RA_EINVAL and nothing is launched.  No hipMalloc, hipFree or allocating
+ * library call.  Every call on a device shares that device's array (no part
+ * of it needs to start at zero; each call writes every entry it reads), so
+ * calls that overlap on one device -- on different streams or host threads
+ * -- race; serialise them. */
+size_t ra_decode_noalloc_max_scratch_bytes(void);
+int ra_decode_attention_noalloc(const void* q, const void* k_pool, const void* v_pool, int64_t pool_slots,
+                                const int32_t* req_to_token, int64_t rtt_rows, int64_t rtt_stride,
+                                const int32_t* req_pool_idx, const int32_t* seq_lens, int32_t batch,
+                                int32_t max_seq_len, int32_t hq, int32_t hkv, int32_t d, float scale,
+                                int32_t num_splits, void* out, hipStream_t stream);
+
 /* Mixed continuous batch (section 3: continuous batching merges new and
  * running requests into one batch; Algorithm 1, B.merge and B.run): the
  * extend requests and the decode requests of one batch in one call, over the

@@ -60,6 +60,9 @@ _SIGS = {
     "ra_decode_chunk_len": ([_i32, _i32, _i32, _i32], _i32),
     "ra_decode_attention": ([_vp, _vp, _vp, _i64, _vp, _i64, _i64, _vp, _vp, _i32, _i32, _i32, _i32, _i32,
                              ctypes.c_float, _i32, _vp, ctypes.c_size_t, _vp, _vp], ctypes.c_int),
+    "ra_decode_noalloc_max_scratch_bytes": ([], ctypes.c_size_t),
+    "ra_decode_attention_noalloc": ([_vp, _vp, _vp, _i64, _vp, _i64, _i64, _vp, _vp, _i32, _i32, _i32, _i32, _i32,
+                                     ctypes.c_float, _i32, _vp, _vp], ctypes.c_int),
     "ra_mixed_attention": ([_vp, _vp, _vp, _i64, _vp, _vp, _vp, _vp, _i32, _i32, _vp,
                             _vp, _vp, _vp, _i32, _i32, _i32, _vp, ctypes.c_size_t, _vp,
                             _vp, _vp, _i64, _vp, _i64, _i64, _i32, _i32, _i32, ctypes.c_float, _vp], ctypes.c_int),
@@ -320,6 +323,28 @@ def ra_decode_attention(q, k_pool, v_pool, req_to_token, req_pool_idx, seq_lens,
         req_to_token.shape[1], _dev(req_pool_idx, torch.int32, "req_pool_idx"),
         _dev(seq_lens, torch.int32, "seq_lens"), b, int(max_seq_len), hq, hkv, d, float(scale), int(num_splits),
         ws_ptr, ws_bytes, _dev(out, torch.bfloat16, "out"), _stream(stream)))
+    return out
+
+
+def ra_decode_noalloc_max_scratch_bytes() -> int:
+    return int(_lib.ra_decode_noalloc_max_scratch_bytes())
+
+
+def ra_decode_attention_noalloc(q, k_pool, v_pool, req_to_token, req_pool_idx, seq_lens, max_seq_len: int,
+                                scale: float, out, num_splits: int = 0, stream=None):
+    """ra_decode_attention without a workspace: the library's per-device
+    scratch holds the split partials.  ``out`` is required (this call
+    allocates nothing)."""
+    import torch
+
+    b, hq, d = q.shape
+    hkv = k_pool.shape[1]
+    _check(_lib.ra_decode_attention_noalloc(
+        _dev(q, torch.bfloat16, "q"), _dev(k_pool, torch.bfloat16, "k_pool"), _dev(v_pool, torch.bfloat16, "v_pool"),
+        k_pool.shape[0], _dev(req_to_token, torch.int32, "req_to_token"), req_to_token.shape[0],
+        req_to_token.shape[1], _dev(req_pool_idx, torch.int32, "req_pool_idx"),
+        _dev(seq_lens, torch.int32, "seq_lens"), b, int(max_seq_len), hq, hkv, d, float(scale), int(num_splits),
+        _dev(out, torch.bfloat16, "out"), _stream(stream)))
     return out
 
 

@@ -26,6 +26,8 @@
 // kernel merges the chunks.  DMAs are issued from inline assembly (the
 // compiler would wait for them before every LDS read); waits are explicit.
 
+#include <mutex>
+
 #include "device_common.h"
 #include "lds_dma.h"
 
@@ -762,4 +764,64 @@ extern "C" int ra_decode_attention(const void* q, const void* k_pool, const void
                        ws_lse, seq_lens, hq, chunk, max_splits, max_seq_len, op);
   }
   return ra_check_launch("ra_decode_attention(combine)");
+}
+
+// ---------------------------------------------------------------------------
+// Allocation-free variant: the split-KV partials live in a file-scope device
+// array instead of a caller workspace.
+// ---------------------------------------------------------------------------
+
+// One copy per device, held until the process ends.  In host code `scratch`
+// names a host-side stand-in, never device memory: kernels receive the
+// address hipGetSymbolAddress reports for the current device.
+constexpr size_t kNoAllocScratchBytes = size_t{128} << 20;
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
+namespace {
+
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[64] = {};
+
+// Device address of this device's scratch, looked up once per device (with
+// that device current, as the caller's calls run).
+int scratch_for_current_device(void** out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64)
+    return ra_fail(RA_EHIP, "ra_decode_attention_noalloc: no usable current device");
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || ptr == nullptr)
+      return ra_fail(RA_EHIP, std::string("ra_decode_attention_noalloc: hipGetSymbolAddress: ") +
+                                  hipGetErrorString(e));
+    g_scratch_ptr[dev] = ptr;
+  }
+  *out = g_scratch_ptr[dev];
+  return RA_OK;
+}
+
+}  // namespace
+
+extern "C" size_t ra_decode_noalloc_max_scratch_bytes(void) { return kNoAllocScratchBytes; }
+
+extern "C" int ra_decode_attention_noalloc(const void* q, const void* k_pool, const void* v_pool, int64_t pool_slots,
+                                           const int32_t* req_to_token, int64_t rtt_rows, int64_t rtt_stride,
+                                           const int32_t* req_pool_idx, const int32_t* seq_lens, int32_t batch,
+                                           int32_t max_seq_len, int32_t hq, int32_t hkv, int32_t d, float scale,
+                                           int32_t num_splits, void* out, hipStream_t stream) {
+  int32_t msl = max_seq_len;
+  if (msl <= 0 && rtt_stride > 0) msl = static_cast<int32_t>(std::min<int64_t>(rtt_stride, INT32_MAX));
+  const size_t need = ra_decode_workspace_bytes(batch, hq, hkv, d, msl, num_splits);
+  if (need > kNoAllocScratchBytes)
+    return ra_fail(RA_EINVAL, "ra_decode_attention_noalloc: the batch needs " + std::to_string(need) +
+                                  " bytes of split scratch, more than the " +
+                                  std::to_string(kNoAllocScratchBytes) + " this entry point holds");
+  void* ws = nullptr;
+  if (need) {
+    const int st = scratch_for_current_device(&ws);
+    if (st != RA_OK) return st;
+  }
+  return ra_decode_attention(q, k_pool, v_pool, pool_slots, req_to_token, rtt_rows, rtt_stride, req_pool_idx,
+                             seq_lens, batch, max_seq_len, hq, hkv, d, scale, num_splits, ws, need, out, stream);
 }
