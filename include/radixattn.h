@@ -175,7 +175,8 @@ int ra_store_kv(const int32_t* slots, const void* k_new, const void* v_new, int6
  *          request r is read from slot req_to_token[req_pool_idx[r] *
  *          rtt_stride + j]; req_to_token is int32 [rtt_rows, rtt_stride]
  *   prefix_lens, extend_lens, extend_start, req_pool_idx: int32 [B]
- *   max_extend_len: host upper bound of extend_lens (sizes the grid)
+ *   max_extend_len: host upper bound of extend_lens (sizes the grid; every
+ *          extend_lens[r] must be <= it: rows past it are never written)
  *   out    [sum E, Hq, D] bf16
  * New token i of request r (position P_r + i) attends positions 0 .. P_r + i.
  * Requires Hq % Hkv == 0, G = Hq / Hkv in {1, 2, 4, 8, 16}, D in {64, 128}.
@@ -231,6 +232,33 @@ int ra_decode_attention_noalloc(const void* q, const void* k_pool, const void* v
                                 const int32_t* req_pool_idx, const int32_t* seq_lens, int32_t batch,
                                 int32_t max_seq_len, int32_t hq, int32_t hkv, int32_t d, float scale,
                                 int32_t num_splits, void* out, hipStream_t stream);
+
+/* Batch validation (a debug aid).  The kernels keep every access inside
+ * the arrays by clamping: a table row outside [0, rtt_rows) reads row 0, a
+ * length above its bound is cut, a slot outside [0, pool_slots) reads the
+ * last slot -- so a caller bug gives plausible but wrong output.  This call
+ * reads the same device arrays and reports such values instead.
+ * Extend (prefix_lens, extend_lens, extend_start non-NULL, seq_lens NULL):
+ * req_pool_idx in [0, rtt_rows), prefix_lens in [0, rtt_stride],
+ * extend_lens in [0, max_extend_len], extend_start + extend_lens within
+ * [0, total_tokens], and every prefix slot req_to_token[row, j < P] in
+ * [0, pool_slots).  Decode (seq_lens non-NULL, the three extend arrays
+ * NULL): req_pool_idx as above, seq_lens in [1, max_seq_len] and every slot
+ * req_to_token[row, j < L] in [0, pool_slots).  Runs a small kernel on
+ * `stream`, waits for the stream, and returns RA_OK or RA_EINVAL with a
+ * message naming the first bad request, the field and, for slots, the
+ * position.  Not for graph capture.  Uses one library-owned device word per
+ * device; concurrent calls on one device are serialised. */
+int ra_check_batch(const int32_t* req_to_token, int64_t rtt_rows, int64_t rtt_stride, int64_t pool_slots,
+                   const int32_t* req_pool_idx, int32_t batch, const int32_t* prefix_lens,
+                   const int32_t* extend_lens, const int32_t* extend_start, int64_t total_tokens,
+                   int32_t max_extend_len, const int32_t* seq_lens, int32_t max_seq_len, hipStream_t stream);
+
+/* Debug switch for the whole library: while enabled (non-zero), every
+ * ra_extend_attention, ra_decode_attention(_noalloc) and ra_mixed_attention
+ * call runs ra_check_batch on its batch first (synchronising the stream) and
+ * returns its error without launching anything.  Off by default. */
+int ra_set_debug_checks(int32_t enable);
 
 /* Mixed continuous batch (section 3: continuous batching merges new and
  * running requests into one batch; Algorithm 1, B.merge and B.run): the

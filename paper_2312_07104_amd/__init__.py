@@ -63,6 +63,8 @@ _SIGS = {
     "ra_decode_noalloc_max_scratch_bytes": ([], ctypes.c_size_t),
     "ra_decode_attention_noalloc": ([_vp, _vp, _vp, _i64, _vp, _i64, _i64, _vp, _vp, _i32, _i32, _i32, _i32, _i32,
                                      ctypes.c_float, _i32, _vp, _vp], ctypes.c_int),
+    "ra_check_batch": ([_vp, _i64, _i64, _i64, _vp, _i32, _vp, _vp, _vp, _i64, _i32, _vp, _i32, _vp], ctypes.c_int),
+    "ra_set_debug_checks": ([_i32], ctypes.c_int),
     "ra_mixed_attention": ([_vp, _vp, _vp, _i64, _vp, _vp, _vp, _vp, _i32, _i32, _vp,
                             _vp, _vp, _vp, _i32, _i32, _i32, _vp, ctypes.c_size_t, _vp,
                             _vp, _vp, _i64, _vp, _i64, _i64, _i32, _i32, _i32, ctypes.c_float, _vp], ctypes.c_int),
@@ -346,6 +348,28 @@ def ra_decode_attention_noalloc(q, k_pool, v_pool, req_to_token, req_pool_idx, s
         _dev(seq_lens, torch.int32, "seq_lens"), b, int(max_seq_len), hq, hkv, d, float(scale), int(num_splits),
         _dev(out, torch.bfloat16, "out"), _stream(stream)))
     return out
+
+
+def ra_check_batch(req_to_token, req_pool_idx, pool_slots: int, prefix_lens=None, extend_lens=None,
+                   extend_start=None, total_tokens: int = 0, max_extend_len: int = 0, seq_lens=None,
+                   max_seq_len: int = 0, stream=None) -> None:
+    """Validates an extend batch (prefix_lens, extend_lens, extend_start) or a
+    decode batch (seq_lens) on the device; raises RadixAttnError naming the
+    first bad request and field."""
+    import torch
+
+    opt = lambda t, n: None if t is None else _dev(t, torch.int32, n)  # noqa: E731
+    _check(_lib.ra_check_batch(
+        _dev(req_to_token, torch.int32, "req_to_token"), req_to_token.shape[0], req_to_token.shape[1],
+        int(pool_slots), _dev(req_pool_idx, torch.int32, "req_pool_idx"), req_pool_idx.shape[0],
+        opt(prefix_lens, "prefix_lens"), opt(extend_lens, "extend_lens"), opt(extend_start, "extend_start"),
+        int(total_tokens), int(max_extend_len), opt(seq_lens, "seq_lens"), int(max_seq_len), _stream(stream)))
+
+
+def ra_set_debug_checks(enable: bool) -> None:
+    """Library-wide debug switch: every attention call validates its batch
+    on the device first (see ra_check_batch)."""
+    _check(_lib.ra_set_debug_checks(1 if enable else 0))
 
 
 def ra_mixed_attention(q_ext, k_new, v_new, req_pool_idx_ext, prefix_lens, extend_lens, extend_start,

@@ -58,12 +58,15 @@ __device__ __forceinline__ bool ra_decode_item(int64_t k, int32_t hkv, int32_t m
 // request's partial last chunk, longest first (lengths in 64 buckets of
 // chunk_len / 64 tokens, ties by request index).  Without it the partial
 // chunks sit among the full ones and a few full chunks start last.  One wave
-// per work-group: it reads the batch's lengths once into `lds` (batch + 130
+// per work-group: it reads the batch's lengths once into `lds` (batch + 129
 // words, the work-group's staging LDS before its first use), counts requests
 // by full chunks and partial chunks by bucket, and finds unit k / hkv with
 // wave scans and ballots.  Returns false past the last unit.
 constexpr int kDecLptMaxBatch = 1536;
 constexpr int kDecLptMaxSplits = 64;
+// Words of LDS the ranking uses: the lengths, the full-chunk histogram
+// (kDecLptMaxSplits + 1 bins) and the partial-chunk histogram (64 bins).
+constexpr int kDecLptWords = kDecLptMaxBatch + kDecLptMaxSplits + 1 + 64;
 
 __device__ __forceinline__ int wave_incl_scan(int v) {
   const int lane = threadIdx.x & 63;
@@ -195,6 +198,7 @@ __global__ __launch_bounds__(64) void decode_partial_kernel(
   constexpr int IDX_AHEAD = NS - 1;
   __shared__ __align__(16) unsigned char kv_lds[NS][2][TILE_B];
   __shared__ __align__(16) int32_t idx_lds[RING][64];
+  static_assert(kDecLptWords * 4 <= sizeof(kv_lds), "ranking scratch exceeds the staging LDS");
 
   int g, split, b;
   if (lpt ? !ra_decode_lpt_item(reinterpret_cast<int32_t*>(&kv_lds[0][0][0]), blockIdx.x, hkv, batch, chunk_len, max_len,
@@ -414,6 +418,7 @@ __global__ __launch_bounds__(64) void decode_partial_vr_kernel(
   constexpr int GROUP_B = TILE * 64;
   constexpr int TILE_B = KS * GROUP_B;
   __shared__ __align__(16) unsigned char v_lds[TILE_B];
+  static_assert(kDecLptWords * 4 <= sizeof(v_lds), "ranking scratch exceeds the staging LDS");
 
   int g, split, b;
   if (lpt ? !ra_decode_lpt_item(reinterpret_cast<int32_t*>(v_lds), blockIdx.x, hkv, batch, chunk_len, max_len,
@@ -713,6 +718,11 @@ extern "C" int ra_decode_attention(const void* q, const void* k_pool, const void
                                      workspace_bytes, out);
   if (st0 != RA_OK || batch == 0) return st0;
   if (max_seq_len <= 0) max_seq_len = static_cast<int32_t>(std::min<int64_t>(rtt_stride, INT32_MAX));
+  if (ra_debug_checks_enabled()) {
+    const int cst = ra_check_batch(req_to_token, rtt_rows, rtt_stride, pool_slots, req_pool_idx, batch, nullptr,
+                                   nullptr, nullptr, 0, 0, seq_lens, max_seq_len, stream);
+    if (cst != RA_OK) return cst;
+  }
   const int32_t grp = hq / hkv;
   const int32_t chunk = ra_decode_chunk_len(batch, hkv, max_seq_len, num_splits);
   const int64_t splits = ceil_div(max_seq_len, chunk);

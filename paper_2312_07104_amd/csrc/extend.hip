@@ -894,6 +894,11 @@ extern "C" int ra_extend_attention(const void* q, const void* k_new, const void*
                                     rtt_stride, req_pool_idx, prefix_lens, extend_lens, extend_start, batch,
                                     max_extend_len, hq, hkv, d, scale, out);
   if (st != RA_OK || batch == 0 || max_extend_len == 0 || total_tokens == 0) return st;
+  if (ra_debug_checks_enabled()) {
+    const int cst = ra_check_batch(req_to_token, rtt_rows, rtt_stride, pool_slots, req_pool_idx, batch, prefix_lens,
+                                   extend_lens, extend_start, total_tokens, max_extend_len, nullptr, 0, stream);
+    if (cst != RA_OK) return cst;
+  }
   const int32_t grp = hq / hkv;
   // At least 256 query rows per kv head (new tokens x query heads per kv
   // head): the 256-row configuration; fewer would leave most of its tile

@@ -3,6 +3,7 @@
 // kernel share the chip instead of running back to back.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <mutex>
 #include <string>
 #include <unordered_map>
@@ -67,6 +68,15 @@ extern "C" int ra_mixed_attention(const void* q_ext, const void* k_new, const vo
                             seq_lens, n_dec, max_seq_len, hq, hkv, d, scale, num_splits, workspace, workspace_bytes,
                             out_dec);
   if (st != RA_OK) return st;
+  if (ra_debug_checks_enabled()) {
+    st = ra_check_batch(req_to_token, rtt_rows, rtt_stride, pool_slots, req_pool_idx_ext, n_ext, prefix_lens,
+                        extend_lens, extend_start, total_tokens, max_extend_len, nullptr, 0, stream);
+    if (st == RA_OK)
+      st = ra_check_batch(req_to_token, rtt_rows, rtt_stride, pool_slots, req_pool_idx_dec, n_dec, nullptr, nullptr,
+                          nullptr, 0, 0, seq_lens, max_seq_len > 0 ? max_seq_len : static_cast<int32_t>(
+                              std::min<int64_t>(rtt_stride, INT32_MAX)), stream);
+    if (st != RA_OK) return st;
+  }
   std::lock_guard<std::mutex> lock(g_mu);
   int device = 0;
   if (hipGetDevice(&device) != hipSuccess) return ra_fail(RA_EHIP, "ra_mixed_attention: hipGetDevice failed");

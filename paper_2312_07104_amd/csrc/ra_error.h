@@ -50,3 +50,6 @@ int ra_decode_validate(const void* q, const void* k_pool, const void* v_pool, in
                        float scale, int32_t num_splits, const void* workspace, size_t workspace_bytes,
                        const void* out);
 
+// True while ra_set_debug_checks(1) is in force: the attention entry points
+// then run ra_check_batch on their batch before launching.
+bool ra_debug_checks_enabled();

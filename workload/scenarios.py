@@ -197,13 +197,13 @@ def cfg4_branching(seed: int = SEED_BASE + 4, n_branch: int = 64, root_len: int 
 
 
 def cfg5_mixed(seed: int = SEED_BASE + 5, n_ext: int = 32, n_dec: int = 512,
-               n_history: int = 18000, pool: int = 4194304, branching: int = 4,
+               n_history: int = 20000, pool: int = 4194304, branching: int = 4,
                ext_p=(1024, 8192), ext_e=(256, 2048), dec_l=(1024, 16384),
                hist_l=(256, 4096), hq: int = 64, hkv: int = 8) -> Scenario:
     """Continuous-batching mix, 70B-like GQA 64/8/128, pool 4194304 slots.
 
     A random segment tree (branching 4, segments U[256, 1024]) drives a
-    history of finished requests (L ~ U[256, 4096], about 100k tree calls),
+    history of 20000 finished requests (L ~ U[256, 4096], 100k tree calls),
     then one batch of 32 extend requests (P ~ U[1024, 8192] along a tree path,
     E ~ U[256, 2048] private) and 512 decode requests (L ~ U[1024, 16384]
     along tree paths).
