@@ -102,36 +102,50 @@ def algorithmic_work(sc, inp):
                 attended=attended, sum_l=sum_l, pairs=pairs)
 
 
-def cpu_baseline(sc, inp, budget_s: float):
-    """The oracle, timed on host cores over a bounded sample of the batch."""
-    from oracle import attention as oa
+def cpu_baseline(sc, inp, budget_s: float, workers: int):
+    """The oracle, timed on the host's cores over a bounded sample of the batch.
+
+    Requests go to a pool of worker processes (spawned, one thread each:
+    OpenMP and BLAS limited to one), the shortest extend request first, then
+    the decode requests in batch order, every worker kept busy until the time
+    budget is spent (running requests finish).  Workers start and import the
+    oracle before the timing starts.  Each request regenerates its inputs from
+    its own token list and attends in float64; regeneration and attention are
+    timed separately inside the workers."""
+    from oracle import pool as opool
 
     try:
         from threadpoolctl import threadpool_info
         blas_threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:  # pragma: no cover
-        blas_threads = 1
-    cores = len(os.sched_getaffinity(0))
-    done_tokens = 0
-    t_start = time.perf_counter()
-    n_ext = n_dec = 0
-    # one extend request (the shortest) then decode requests until the budget is spent
+        blas_threads = None
+    tasks, ctx, flops = [], [], []
     if inp.ext_meta:
         toks, p, e, _ = min(inp.ext_meta, key=lambda m: m[2] * (m[1] + m[2]))
-        oa.extend_reference(toks, p, e, sc.seed, sc.hq, sc.hkv, sc.d, sc.scale)
-        done_tokens += p + e
-        n_ext += 1
+        tasks.append(opool.extend_task(toks, p, e, sc.seed, sc.hq, sc.hkv, sc.d, sc.scale))
+        ctx.append(p + e)
+        flops.append(4.0 * sc.d * sc.hq * (e * p + e * (e + 1) // 2))
     for toks, l in inp.dec_meta:
-        if time.perf_counter() - t_start > budget_s:
-            break
-        oa.decode_reference(toks, l, sc.seed, sc.hq, sc.hkv, sc.d, sc.scale)
-        done_tokens += l
-        n_dec += 1
-    dt = time.perf_counter() - t_start
-    return {"value": done_tokens / dt, "unit": "attended KV tokens/s", "cores": max(cores, blas_threads),
-            "kind": "oracle",
-            "sample": f"{n_ext} extend + {n_dec} decode requests of the batch "
-                      f"({done_tokens} context tokens, {dt:.1f} s, inputs regenerated inside the timing)"}
+        tasks.append(opool.decode_task(toks, l, sc.seed, sc.hq, sc.hkv, sc.d, sc.scale))
+        ctx.append(l)
+        flops.append(4.0 * sc.d * sc.hq * l)
+    with opool.OraclePool(workers, threads_per_worker=1) as pool:
+        pool.warm()
+        done, wall = pool.run_for(tasks, budget_s)
+    idx = [i for i, _, _ in done]
+    tokens = sum(ctx[i] for i in idx)
+    n_ext = sum(1 for i in idx if inp.ext_meta and i == 0)
+    regen = sum(tm.get("regen", 0.0) for _, _, tm in done)
+    attend = sum(tm.get("attend", 0.0) for _, _, tm in done)
+    return {"value": tokens / wall, "unit": "attended KV tokens/s", "cores": workers, "kind": "oracle",
+            "processes": workers, "threads_per_process": 1, "affinity_cores": len(os.sched_getaffinity(0)),
+            "blas_threads_in_parent": blas_threads,
+            "gflops": sum(flops[i] for i in idx) / wall / 1e9,
+            "wall_s": wall, "regen_cpu_s": regen, "attend_cpu_s": attend,
+            "sample": f"{n_ext} extend + {len(idx) - n_ext} decode requests of the batch ({tokens} context tokens "
+                      f"in {wall:.1f} s on {workers} worker processes of one thread each; each request "
+                      f"regenerates its inputs from its token list: {regen:.0f} CPU-s regeneration, "
+                      f"{attend:.0f} CPU-s float64 attention)"}
 
 
 def scheduler_report(sc, n: int = 300):
@@ -203,6 +217,9 @@ def main():
                     help="batch of the workload to time; earlier batches run and finish first (their new tokens "
                          "are stored and their sequences inserted)")
     ap.add_argument("--cpu-budget", type=float, default=20.0)
+    ap.add_argument("--cpu-workers", type=int, default=max(1, min(16, len(os.sched_getaffinity(0)))),
+                    help="oracle worker processes for the CPU baseline (one thread each)")
+    ap.add_argument("--no-peaks", action="store_true", help="skip the machine-peak microbenchmarks")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="after the timed loop, run one device copy of this size (HBM counter calibration)")
@@ -329,6 +346,28 @@ def main():
         if r:
             r["frac"] = r["achieved"] / r["peak"]
             r["traffic"] = measured_traffic(r["kernel"], sc.name)
+            # HBM bytes the counters saw per launch over the kernel's duration
+            if r["traffic"]:
+                r["hbm_gbs"] = r["traffic"] / (kernels[r["kernel"]]["ms"] * 1e-3) / 1e9
+                r["hbm_frac"] = r["hbm_gbs"] / HBM_PEAK_GBS
+
+    peaks = None
+    if not args.no_peaks:
+        from workload import peaks as pk
+
+        log("[bench] measuring machine peaks (streaming read, 256-byte gather, MFMA loops)")
+        peaks = pk.measure()
+        for r in (roof, other):
+            if not r:
+                continue
+            if r["unit"] == "TFLOP/s":
+                r["measured_peak"] = peaks["mfma16_bf16_tflops"]
+                r["frac_of_measured"] = r["achieved"] / r["measured_peak"]
+            else:
+                r["measured_peak"] = peaks["gather256_gbs"]
+                r["frac_of_measured"] = r["achieved"] / r["measured_peak"]
+                if r.get("hbm_gbs"):
+                    r["hbm_frac_of_measured"] = r["hbm_gbs"] / r["measured_peak"]
 
     if args.copy_calibration_mib:
         n = args.copy_calibration_mib << 20
@@ -354,6 +393,7 @@ def main():
         "ms_per_step_sequential_cold": ms_seq,
         "roofline": roof,
         "roofline_other": other,
+        "peaks_measured": peaks,
         "kernels": kernels,
         "host_tree": {"calls": run.history_ops, "seconds": run.history_seconds,
                       "calls_per_s": run.history_ops / max(run.history_seconds, 1e-9),
@@ -363,7 +403,7 @@ def main():
     line["data_parallel"] = data_parallel_report(sc)
     if not args.no_cpu_baseline:
         log("[bench] timing the oracle on host cores")
-        line["cpu_baseline"] = cpu_baseline(sc, inp, args.cpu_budget)
+        line["cpu_baseline"] = cpu_baseline(sc, inp, args.cpu_budget, args.cpu_workers)
     print(json.dumps(line), flush=True)
 
 

@@ -18,6 +18,7 @@ from __future__ import annotations
 import concurrent.futures as cf
 import multiprocessing as mp
 import os
+import time
 
 import numpy as np
 
@@ -93,6 +94,38 @@ class OraclePool:
         for f in cf.as_completed(futs):
             out, tm = f.result()
             yield futs[f], out, tm
+
+    def warm(self) -> None:
+        """Starts every worker and imports the oracle in it (a tiny task per
+        worker), so that later timings exclude interpreter start-up."""
+        tiny = decode_task(np.arange(4, dtype=np.int32), 4, 1, 1, 1, 16, 0.25)
+        list(self.imap([tiny] * (2 * self.workers)))
+
+    def run_for(self, tasks, seconds: float):
+        """Runs tasks in order with every worker busy and stops submitting
+        new ones once ``seconds`` have passed (running ones finish).
+        Returns ([(index, result, timings)], wall seconds)."""
+        t0 = time.perf_counter()
+        it = iter(enumerate(tasks))
+        pending = {}
+
+        def submit() -> None:
+            nxt = next(it, None)
+            if nxt is not None:
+                pending[self._ex.submit(_run_task, nxt[1])] = nxt[0]
+
+        for _ in range(self.workers):
+            submit()
+        done = []
+        while pending:
+            fin, _ = cf.wait(pending, return_when=cf.FIRST_COMPLETED)
+            for f in fin:
+                i = pending.pop(f)
+                out, tm = f.result()
+                done.append((i, out, tm))
+                if time.perf_counter() - t0 < seconds:
+                    submit()
+        return done, time.perf_counter() - t0
 
     def map(self, tasks) -> list:
         res = [None] * len(tasks)

@@ -1,0 +1,119 @@
+// Machine-peak microbenchmarks for the roofline report (bench.py --peaks):
+// the HBM read bandwidth a streaming kernel reaches, the bandwidth of random
+// 256-byte row gathers (the access pattern of attention over a pool of
+// one-token pages), and the bf16 rate of a loop of matrix-core instructions.
+// They compute no attention; each folds what it reads into one word per
+// thread so the compiler keeps every load.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+typedef __bf16 pk_bf16x8 __attribute__((ext_vector_type(8)));
+typedef float pk_f32x4 __attribute__((ext_vector_type(4)));
+typedef float pk_f32x16 __attribute__((ext_vector_type(16)));
+
+__device__ __forceinline__ uint32_t pk_fold(uint4 v) { return v.x ^ v.y ^ v.z ^ v.w; }
+
+// Streaming read of n16 16-byte words, grid-stride, four loads in flight per
+// thread.
+__global__ __launch_bounds__(256) void pk_read_kernel(const uint4* __restrict__ src, int64_t n16,
+                                                      uint32_t* __restrict__ sink) {
+  const int64_t stride = static_cast<int64_t>(gridDim.x) * 256;
+  int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  uint32_t acc = 0;
+  for (; i + 3 * stride < n16; i += 4 * stride) {
+    const uint4 a = src[i], b = src[i + stride], c = src[i + 2 * stride], d = src[i + 3 * stride];
+    acc ^= pk_fold(a) ^ pk_fold(b) ^ pk_fold(c) ^ pk_fold(d);
+  }
+  for (; i < n16; i += stride) acc ^= pk_fold(src[i]);
+  sink[static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x] = acc;
+}
+
+// Random row gather: row r is the 256-byte head row (r % heads) of slot
+// slots[r] in a pool of slot_bytes-byte slots.  Sixteen lanes read one row
+// (16 bytes each), so a wave instruction reads four rows; each wave walks its
+// own run of rows, sixteen rows (four instructions) in flight.
+__global__ __launch_bounds__(256) void pk_gather_kernel(const unsigned char* __restrict__ pool,
+                                                        const int32_t* __restrict__ slots, int64_t n_rows,
+                                                        int32_t heads, int32_t slot_bytes,
+                                                        uint32_t* __restrict__ sink) {
+  const int lane = threadIdx.x & 63;
+  const int64_t wave = (static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x) >> 6;
+  const int64_t n_waves = static_cast<int64_t>(gridDim.x) * 4;
+  const int64_t per_wave = (n_rows + n_waves - 1) / n_waves;
+  const int64_t r0 = wave * per_wave;
+  const int64_t r1 = r0 + per_wave < n_rows ? r0 + per_wave : n_rows;
+  uint32_t acc = 0;
+  for (int64_t r = r0; r < r1; r += 16) {
+    uint4 v[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      int64_t row = r + 4 * k + (lane >> 4);
+      row = row < r1 ? row : r1 - 1;
+      const int64_t off = static_cast<int64_t>(slots[row]) * slot_bytes + (row % heads) * 256 + (lane & 15) * 16;
+      v[k] = *reinterpret_cast<const uint4*>(pool + off);
+    }
+#pragma unroll
+    for (int k = 0; k < 4; ++k) acc ^= pk_fold(v[k]);
+  }
+  sink[static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x] = acc;
+}
+
+// Matrix-core loop: four independent accumulator chains per wave of
+// 16x16x32 bf16 MFMAs (16384 flops each) on register operands.
+__global__ __launch_bounds__(256) void pk_mfma16_kernel(int32_t iters, float* __restrict__ sink) {
+  const int lane = threadIdx.x & 63;
+  pk_bf16x8 a, b;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    a[i] = static_cast<__bf16>(0.001f * (lane + i));
+    b[i] = static_cast<__bf16>(0.002f * (lane - i));
+  }
+  pk_f32x4 c0 = {0.f, 0.f, 0.f, 0.f}, c1 = c0, c2 = c0, c3 = c0;
+  for (int it = 0; it < iters; ++it) {
+    c0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c0, 0, 0, 0);
+    c1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c1, 0, 0, 0);
+    c2 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c2, 0, 0, 0);
+    c3 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c3, 0, 0, 0);
+  }
+  sink[static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x] = c0[0] + c1[1] + c2[2] + c3[3];
+}
+
+// The same with 32x32x16 bf16 MFMAs (32768 flops each).
+__global__ __launch_bounds__(256) void pk_mfma32_kernel(int32_t iters, float* __restrict__ sink) {
+  const int lane = threadIdx.x & 63;
+  pk_bf16x8 a, b;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    a[i] = static_cast<__bf16>(0.001f * (lane + i));
+    b[i] = static_cast<__bf16>(0.002f * (lane - i));
+  }
+  pk_f32x16 c0 = {}, c1 = {}, c2 = {}, c3 = {};
+  for (int it = 0; it < iters; ++it) {
+    c0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c0, 0, 0, 0);
+    c1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c1, 0, 0, 0);
+    c2 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c2, 0, 0, 0);
+    c3 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c3, 0, 0, 0);
+  }
+  sink[static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x] = c0[0] + c1[1] + c2[2] + c3[3];
+}
+
+extern "C" int pk_read(const void* src, int64_t bytes, void* sink, int32_t blocks, hipStream_t s) {
+  hipLaunchKernelGGL(pk_read_kernel, dim3(blocks), dim3(256), 0, s, static_cast<const uint4*>(src), bytes / 16,
+                     static_cast<uint32_t*>(sink));
+  return hipGetLastError() == hipSuccess ? 0 : -3;
+}
+
+extern "C" int pk_gather(const void* pool, const int32_t* slots, int64_t n_rows, int32_t heads, int32_t slot_bytes,
+                         void* sink, int32_t blocks, hipStream_t s) {
+  hipLaunchKernelGGL(pk_gather_kernel, dim3(blocks), dim3(256), 0, s, static_cast<const unsigned char*>(pool), slots,
+                     n_rows, heads, slot_bytes, static_cast<uint32_t*>(sink));
+  return hipGetLastError() == hipSuccess ? 0 : -3;
+}
+
+extern "C" int pk_mfma(int32_t shape, int32_t iters, void* sink, int32_t blocks, hipStream_t s) {
+  if (shape == 16)
+    hipLaunchKernelGGL(pk_mfma16_kernel, dim3(blocks), dim3(256), 0, s, iters, static_cast<float*>(sink));
+  else
+    hipLaunchKernelGGL(pk_mfma32_kernel, dim3(blocks), dim3(256), 0, s, iters, static_cast<float*>(sink));
+  return hipGetLastError() == hipSuccess ? 0 : -3;
+}
