@@ -361,10 +361,10 @@ def main():
             if not r:
                 continue
             if r["unit"] == "TFLOP/s":
-                r["measured_peak"] = peaks["mfma16_bf16_tflops"]
+                r["measured_peak"] = max(peaks["mfma16_bf16_tflops"], peaks["mfma32_bf16_tflops"])
                 r["frac_of_measured"] = r["achieved"] / r["measured_peak"]
             else:
-                r["measured_peak"] = peaks["gather256_gbs"]
+                r["measured_peak"] = max(peaks["gather256_gbs"], peaks["hbm_read_gbs"])
                 r["frac_of_measured"] = r["achieved"] / r["measured_peak"]
                 if r.get("hbm_gbs"):
                     r["hbm_frac_of_measured"] = r["hbm_gbs"] / r["measured_peak"]

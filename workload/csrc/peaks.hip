@@ -7,6 +7,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 typedef __bf16 pk_bf16x8 __attribute__((ext_vector_type(8)));
 typedef float pk_f32x4 __attribute__((ext_vector_type(4)));
 typedef float pk_f32x16 __attribute__((ext_vector_type(16)));
@@ -58,9 +60,15 @@ __global__ __launch_bounds__(256) void pk_gather_kernel(const unsigned char* __r
   sink[static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x] = acc;
 }
 
-// Matrix-core loop: four independent accumulator chains per wave of
-// 16x16x32 bf16 MFMAs (16384 flops each) on register operands.
-__global__ __launch_bounds__(256) void pk_mfma16_kernel(int32_t iters, float* __restrict__ sink) {
+// Matrix-core loop: eight independent accumulator chains per wave of bf16
+// MFMAs on register operands, one wave per SIMD (one 256-thread work-group
+// per CU), so each wave's cycles are its SIMD's.  SHAPE 16: 16x16x32
+// (16384 flops per instruction); SHAPE 32: 32x32x16 (32768).  Lane 0 of
+// each wave records the loop's shader-clock cycles and real-time ticks.
+template <int SHAPE>
+__global__ __launch_bounds__(256) void pk_mfma_kernel(int32_t iters, float* __restrict__ sink,
+                                                      uint64_t* __restrict__ clocks) {
+  typedef typename std::conditional<SHAPE == 16, pk_f32x4, pk_f32x16>::type acc_t;
   const int lane = threadIdx.x & 63;
   pk_bf16x8 a, b;
 #pragma unroll
@@ -68,33 +76,31 @@ __global__ __launch_bounds__(256) void pk_mfma16_kernel(int32_t iters, float* __
     a[i] = static_cast<__bf16>(0.001f * (lane + i));
     b[i] = static_cast<__bf16>(0.002f * (lane - i));
   }
-  pk_f32x4 c0 = {0.f, 0.f, 0.f, 0.f}, c1 = c0, c2 = c0, c3 = c0;
-  for (int it = 0; it < iters; ++it) {
-    c0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c0, 0, 0, 0);
-    c1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c1, 0, 0, 0);
-    c2 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c2, 0, 0, 0);
-    c3 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c3, 0, 0, 0);
-  }
-  sink[static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x] = c0[0] + c1[1] + c2[2] + c3[3];
-}
-
-// The same with 32x32x16 bf16 MFMAs (32768 flops each).
-__global__ __launch_bounds__(256) void pk_mfma32_kernel(int32_t iters, float* __restrict__ sink) {
-  const int lane = threadIdx.x & 63;
-  pk_bf16x8 a, b;
+  acc_t c[8];
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    a[i] = static_cast<__bf16>(0.001f * (lane + i));
-    b[i] = static_cast<__bf16>(0.002f * (lane - i));
-  }
-  pk_f32x16 c0 = {}, c1 = {}, c2 = {}, c3 = {};
+  for (int k = 0; k < 8; ++k) c[k] = acc_t{};
+  const uint64_t t0 = __builtin_amdgcn_s_memtime(), r0 = __builtin_amdgcn_s_memrealtime();
   for (int it = 0; it < iters; ++it) {
-    c0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c0, 0, 0, 0);
-    c1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c1, 0, 0, 0);
-    c2 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c2, 0, 0, 0);
-    c3 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c3, 0, 0, 0);
+    // inline assembly keeps each accumulator in place (the compiler's own
+    // MFMAs here came with register moves between them)
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      if constexpr (SHAPE == 16) asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0" : "+a"(c[k]) : "v"(a), "v"(b));
+      else asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(c[k]) : "v"(a), "v"(b));
+    }
   }
-  sink[static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x] = c0[0] + c1[1] + c2[2] + c3[3];
+  // wait states before the VALU reads the last MFMAs' results
+  asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" ::: "memory");
+  float r = 0.f;
+#pragma unroll
+  for (int k = 0; k < 8; ++k) r += c[k][0];
+  sink[static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x] = r;
+  const uint64_t t1 = __builtin_amdgcn_s_memtime(), r1 = __builtin_amdgcn_s_memrealtime();
+  if (lane == 0) {
+    const int64_t w = (static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x) >> 6;
+    clocks[2 * w] = t1 - t0;      // shader clock cycles of this wave's loop
+    clocks[2 * w + 1] = r1 - r0;  // 100 MHz real-time ticks
+  }
 }
 
 extern "C" int pk_read(const void* src, int64_t bytes, void* sink, int32_t blocks, hipStream_t s) {
@@ -110,10 +116,12 @@ extern "C" int pk_gather(const void* pool, const int32_t* slots, int64_t n_rows,
   return hipGetLastError() == hipSuccess ? 0 : -3;
 }
 
-extern "C" int pk_mfma(int32_t shape, int32_t iters, void* sink, int32_t blocks, hipStream_t s) {
+extern "C" int pk_mfma(int32_t shape, int32_t iters, void* sink, void* clocks, int32_t blocks, hipStream_t s) {
   if (shape == 16)
-    hipLaunchKernelGGL(pk_mfma16_kernel, dim3(blocks), dim3(256), 0, s, iters, static_cast<float*>(sink));
+    hipLaunchKernelGGL(pk_mfma_kernel<16>, dim3(blocks), dim3(256), 0, s, iters, static_cast<float*>(sink),
+                       static_cast<uint64_t*>(clocks));
   else
-    hipLaunchKernelGGL(pk_mfma32_kernel, dim3(blocks), dim3(256), 0, s, iters, static_cast<float*>(sink));
+    hipLaunchKernelGGL(pk_mfma_kernel<32>, dim3(blocks), dim3(256), 0, s, iters, static_cast<float*>(sink),
+                       static_cast<uint64_t*>(clocks));
   return hipGetLastError() == hipSuccess ? 0 : -3;
 }

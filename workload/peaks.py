@@ -5,7 +5,8 @@
   2 KiB slots (8 heads x 128 x bf16), the access pattern of decode over a
   pool of one-token pages.
 * ``mfma16_bf16_tflops`` / ``mfma32_bf16_tflops``: loops of 16x16x32 and
-  32x32x16 bf16 MFMAs, four independent chains per wave, four waves per SIMD.
+  32x32x16 bf16 MFMAs, eight independent chains per wave, one wave per SIMD;
+  with the cycles per instruction and the shader clock each wave measured.
 
 Each figure is the median of several launches timed with HIP events on the
 stream the kernels run on.  No attention is computed here.
@@ -27,7 +28,7 @@ def _lib():
     vp, i64, i32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32
     lib.pk_read.argtypes = [vp, i64, vp, i32, vp]
     lib.pk_gather.argtypes = [vp, vp, i64, i32, i32, vp, i32, vp]
-    lib.pk_mfma.argtypes = [i32, i32, vp, i32, vp]
+    lib.pk_mfma.argtypes = [i32, i32, vp, vp, i32, vp]
     for f in (lib.pk_read, lib.pk_gather, lib.pk_mfma):
         f.restype = ctypes.c_int
     return lib
@@ -81,11 +82,16 @@ def measure(reps: int = 7, read_gib: int = 4, pool_gib: int = 8, gather_rows: in
     out["gather256_gbs"] = gather_rows * 256 / (ms * 1e-3) / 1e9
     del pool, slots
 
-    mblocks = cus * 4
+    mblocks = cus  # one 256-thread work-group per CU: one wave per SIMD
     fsink = torch.empty(mblocks * 256, dtype=torch.float32, device=dev)
+    clocks = torch.zeros((mblocks * 4, 2), dtype=torch.int64, device=dev)
     for shape, flops in ((16, 16 * 16 * 32 * 2), (32, 32 * 32 * 16 * 2)):
-        ms = _timed(lambda s: chk(lib.pk_mfma(shape, mfma_iters, fsink.data_ptr(), mblocks, s.cuda_stream)), reps)
-        total = mblocks * 4 * mfma_iters * 4 * flops
+        ms = _timed(lambda s: chk(lib.pk_mfma(shape, mfma_iters, fsink.data_ptr(), clocks.data_ptr(), mblocks,
+                                              s.cuda_stream)), reps)
+        total = mblocks * 4 * mfma_iters * 8 * flops
         out[f"mfma{shape}_bf16_tflops"] = total / (ms * 1e-3) / 1e12
+        c = clocks.cpu().numpy().astype(np.float64)
+        out[f"mfma{shape}_cycles_per_instr"] = float(np.median(c[:, 0]) / (8 * mfma_iters))
+        out[f"mfma{shape}_shader_ghz"] = float(np.median(c[:, 0] / (c[:, 1] / 100e6)) / 1e9)
     torch.cuda.synchronize()
     return out
