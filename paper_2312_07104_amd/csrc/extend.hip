@@ -94,11 +94,12 @@ constexpr int kLptMaxBatch = 1016;
 // come back through `req_args`, read once for the whole batch.  The LDS loops
 // read four words per instruction so that their latencies overlap.  Returns
 // false when block k has no unit.
+template <bool UNIFORM>
 __device__ bool ra_lpt_item(int32_t* scratch, int64_t k, int32_t hkv, int32_t batch, int32_t tpb,
                             const int32_t* __restrict__ req_pool_idx, const int32_t* __restrict__ prefix_lens,
                             const int32_t* __restrict__ extend_lens, const int32_t* __restrict__ extend_start,
                             int64_t total_tokens, int64_t rtt_stride, int& g, int& b, int& qt,
-                            int32_t (&req_args)[4]) {
+                            int32_t (&req_args)[4], int nthreads) {
   const int bp = (batch + 3) & ~3;         // batch padded to whole int4 reads
   int32_t* args = scratch;                 // [batch][4] start, E, P, table row as passed (16-byte entries)
   int32_t* cost = scratch + 4 * batch;     // [bp] key count of the request's units, -1 if none, -2 padding
@@ -106,7 +107,7 @@ __device__ bool ra_lpt_item(int32_t* scratch, int64_t k, int32_t hkv, int32_t ba
   int32_t* nrank = nun + batch;            // [bp] units by rank (0 padding)
   int32_t* ord = nrank + bp;               // [batch] request at each rank
   int32_t* found = ord + batch;            // [2] request and unit offset of this block
-  const int tid = threadIdx.x, nt = blockDim.x;
+  const int tid = static_cast<int>(UNIFORM ? __builtin_amdgcn_workitem_id_x() : threadIdx.x), nt = nthreads;
   if (tid == 0) found[0] = -1;
   for (int t = tid; t < bp; t += nt) {
     if (t >= batch) {
@@ -123,32 +124,20 @@ __device__ bool ra_lpt_item(int32_t* scratch, int64_t k, int32_t hkv, int32_t ba
     cost[t] = nu > 0 ? static_cast<int32_t>(min<int64_t>(p + e, INT32_MAX)) : -1;
   }
   __syncthreads();
-  // rank = requests with a larger key count, or an equal one and a smaller index
-  int32_t rk[4], nu_own[4];  // batch <= kLptMaxBatch <= 4 * blockDim.x
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int t = tid + i * nt;
-    rk[i] = -1;
-    if (t < batch) {
-      const int32_t c = cost[t];
-      int rank = 0;
-      for (int s4 = 0; s4 < bp; s4 += 4) {
-        const int4 cs = *reinterpret_cast<const int4*>(&cost[s4]);
-        rank += (cs.x > c) | ((cs.x == c) & (s4 < t));
-        rank += (cs.y > c) | ((cs.y == c) & (s4 + 1 < t));
-        rank += (cs.z > c) | ((cs.z == c) & (s4 + 2 < t));
-        rank += (cs.w > c) | ((cs.w == c) & (s4 + 3 < t));
-      }
-      rk[i] = rank;
-      nu_own[i] = nun[t];
+  // rank = requests with a larger key count, or an equal one and a smaller
+  // index (cost is only read here; ord and nrank are other words)
+  for (int t = tid; t < batch; t += nt) {
+    const int32_t c = cost[t];
+    int rank = 0;
+    for (int s4 = 0; s4 < bp; s4 += 4) {
+      const int4 cs = *reinterpret_cast<const int4*>(&cost[s4]);
+      rank += (cs.x > c) | ((cs.x == c) & (s4 < t));
+      rank += (cs.y > c) | ((cs.y == c) & (s4 + 1 < t));
+      rank += (cs.z > c) | ((cs.z == c) & (s4 + 2 < t));
+      rank += (cs.w > c) | ((cs.w == c) & (s4 + 3 < t));
     }
-  }
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    if (rk[i] >= 0) {
-      ord[rk[i]] = tid + i * nt;
-      nrank[rk[i]] = nu_own[i];
-    }
+    ord[rank] = t;
+    nrank[rank] = nun[t];
   }
   __syncthreads();
   // Wave 0 scans the unit counts in rank order, 64 ranks at a time, and
@@ -174,11 +163,14 @@ __device__ bool ra_lpt_item(int32_t* scratch, int64_t k, int32_t hkv, int32_t ba
     }
   }
   __syncthreads();
-  const int req = found[0];
-  const int tile = found[1];
+  // Every lane reads the same words.  UNIFORM makes that known to the
+  // compiler, so the item's sizes, loops and branches stay scalar.
+  auto uni = [](int32_t v) { return UNIFORM ? __builtin_amdgcn_readfirstlane(v) : v; };
+  const int req = uni(found[0]);
+  const int tile = uni(found[1]);
   if (req >= 0) {
     const int4 a = *reinterpret_cast<const int4*>(&args[4 * req]);
-    req_args[0] = a.x, req_args[1] = a.y, req_args[2] = a.z, req_args[3] = a.w;
+    req_args[0] = uni(a.x), req_args[1] = uni(a.y), req_args[2] = uni(a.z), req_args[3] = uni(a.w);
   }
   // the scratch is the K/V ring, which the copies overwrite next
   __syncthreads();
@@ -221,19 +213,29 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void extend_kernel(
   // Work-groups go to the 8 XCDs round-robin (block i -> XCD i % 8).  Either
   // order below keeps the blocks of one kv head together on an XCD where it
   // can, so they share K/V rows through its L2.
+  // The 256-row shape reads its ids through the intrinsics rather than
+  // blockIdx / threadIdx: in a kernel this large the helper calls behind
+  // those are not always inlined, and their results then look per-lane to
+  // the compiler, which turns the item's loops and branches into divergent
+  // ones (ten more VALU instructions per fused step).  The 128-row shape
+  // keeps the helpers: with scalar loops its register allocation moves O^T
+  // accumulators next to the inline-assembly MFMAs, which the wait-state
+  // check on its assembly rejects.
+  constexpr bool kUniform = WAVES == 8;
+  const int64_t blk = kUniform ? static_cast<int64_t>(__builtin_amdgcn_workgroup_id_x()) : blockIdx.x;
   const int tpb = kBM / grp;  // new tokens per tile
   const int64_t n_items = static_cast<int64_t>(hkv) * batch * n_qtiles;
   int g, b, qt;
   int32_t req_args[4];  // extend_start, extend_lens, prefix_lens, req_pool_idx of request b
   if (lpt) {
-    if (!ra_lpt_item(reinterpret_cast<int32_t*>(kv_lds), blockIdx.x, hkv, batch, tpb, req_pool_idx, prefix_lens,
-                     extend_lens, extend_start, total_tokens, rtt_stride, g, b, qt, req_args))
+    if (!ra_lpt_item<kUniform>(reinterpret_cast<int32_t*>(kv_lds), blk, hkv, batch, tpb, req_pool_idx, prefix_lens,
+                     extend_lens, extend_start, total_tokens, rtt_stride, g, b, qt, req_args, WAVES * 64))
       return;
   } else {
     // Static order: XCD i % 8 takes a contiguous eighth of the (kv head,
     // request, query tile) order.
     const int64_t per_xcd = (n_items + 7) / 8;
-    const int64_t item = static_cast<int64_t>(blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
+    const int64_t item = (blk % 8) * per_xcd + blk / 8;
     if (item >= n_items) return;
     g = static_cast<int>(item / (static_cast<int64_t>(batch) * n_qtiles));
     const int rem = static_cast<int>(item % (static_cast<int64_t>(batch) * n_qtiles));
@@ -245,7 +247,7 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void extend_kernel(
 
   const int64_t start = req_args[0];
   int64_t E = req_args[1];
-  if (start < 0 || start > total_tokens) return;
+  if (qt < 0 || qt >= n_qtiles || start < 0 || start > total_tokens) return;
   E = min(E, total_tokens - start);
   const int tok0 = qt * tpb;
   if (E <= 0 || tok0 >= E) return;
@@ -258,7 +260,7 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void extend_kernel(
   const int hq = hkv * grp;
   const int n_tiles = (kend + kBN - 1) / kBN;
 
-  const int tid = threadIdx.x;
+  const int tid = static_cast<int>(kUniform ? __builtin_amdgcn_workitem_id_x() : threadIdx.x);
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform (SGPR)
   const int lane = tid & 63;
   const int c = lane & 15;

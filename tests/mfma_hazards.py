@@ -3,19 +3,22 @@
 The extend kernel issues its MFMAs from inline assembly, and the compiler
 inserts no wait states around inline assembly, so the kernel keeps them by
 itself (s_nop runs, instruction order).  This checker scans the assembly of
-each kernel for the dependency rules that the hardware does not interlock
-for 8-pass XDL instructions (v_mfma_f32_16x16x32_bf16), counting wait states
-conservatively (one per instruction, N + 1 for s_nop N) along every
-control-flow path, loops included:
+each kernel for the dependency rules that the hardware does not interlock,
+counting wait states conservatively (one per instruction, N + 1 for s_nop N)
+along every control-flow path, loops included.  The counts depend on the
+instruction's pass count: v_mfma_f32_16x16x32_bf16 (16 cycles) and
+v_mfma_f32_32x32x16_bf16 (32 cycles, 8 passes):
 
 * VALU write of a register, then an MFMA reading it (A, B or C): 2.
 * MFMA write of a register, then a VALU, LDS or memory instruction reading
-  or writing it: 11 (the value is not there yet).
-* MFMA write of a register, then an MFMA reading it as A or B: 11.
+  or writing it: 11 (16x16x32) or 12 (32x32x16; the compiler itself puts
+  s_nop 11 after such an MFMA) -- the value is not there yet.
+* MFMA write of a register, then an MFMA reading it as A or B: the same.
   (Reading it as C with the identical register range is the accumulation
   chain, which the hardware forwards.)
 * MFMA read of its C operand, then a VALU, LDS or memory instruction writing
-  that register: 7 (the operand is read some passes after issue).
+  that register: 7 (16x16x32) or 11 (32x32x16) -- the operand is read some
+  passes after issue.
 
 Used by tests/test_kernel_hazards.py; it reads text only.
 """
@@ -27,6 +30,12 @@ from dataclasses import dataclass, field
 VALU_MFMA = 2
 MFMA_READ = 11
 MFMA_SRCC_WAR = 7
+# per-opcode (result-read, C-operand write-after-read) wait states
+_WAITS = {"v_mfma_f32_32x32x16_bf16": (12, 11)}
+
+
+def _waits(op: str) -> tuple[int, int]:
+    return _WAITS.get(op, (MFMA_READ, MFMA_SRCC_WAR))
 
 _REG = re.compile(r"^([va])(?:\[(\d+):(\d+)\]|(\d+))$")
 
@@ -147,21 +156,22 @@ def check(ins: list[Ins]) -> list[str]:
             if not pj.mfma and pj.defs & it.uses:
                 out.append(f"VALU write -> MFMA read within {VALU_MFMA}: {pj.text} -> {it.text}")
             stack.extend((p, w + pj.ws) for p in preds.get(j, []))
-        for j in _forward(ins, i, MFMA_READ):
+        read_ws, war_ws = _waits(it.op)
+        for j in _forward(ins, i, read_ws):
             nj = ins[j]
             if nj.mfma:
                 if nj.srcab & it.defs:
-                    out.append(f"MFMA write -> MFMA A/B read within {MFMA_READ}: {it.text} -> {nj.text}")
+                    out.append(f"MFMA write -> MFMA A/B read within {read_ws}: {it.text} -> {nj.text}")
                 if nj.srcc & it.defs and nj.srcc != it.defs:
-                    out.append(f"MFMA write -> partial C read within {MFMA_READ}: {it.text} -> {nj.text}")
+                    out.append(f"MFMA write -> partial C read within {read_ws}: {it.text} -> {nj.text}")
                 continue
             if (nj.uses | nj.defs) & it.defs:
-                out.append(f"MFMA write -> access within {MFMA_READ}: {it.text} -> {nj.text}")
+                out.append(f"MFMA write -> access within {read_ws}: {it.text} -> {nj.text}")
         if it.srcc and it.srcc != it.defs:
-            for j in _forward(ins, i, MFMA_SRCC_WAR):
+            for j in _forward(ins, i, war_ws):
                 nj = ins[j]
                 if not nj.mfma and nj.defs & it.srcc:
-                    out.append(f"MFMA C read -> write within {MFMA_SRCC_WAR}: {it.text} -> {nj.text}")
+                    out.append(f"MFMA C read -> write within {war_ws}: {it.text} -> {nj.text}")
     return out
 
 
@@ -178,7 +188,10 @@ def kernels(asm_text: str) -> dict[str, list[str]]:
             out[name] = []
             continue
         if name is not None:
-            out[name].append(line)
-            if line.strip().startswith("s_endpgm"):
+            # a kernel may hold several s_endpgm (early exits); its body ends
+            # at the function's end label
+            if line.strip().startswith(".Lfunc_end"):
                 name = None
+                continue
+            out[name].append(line)
     return out

@@ -70,6 +70,28 @@ def test_checker_flags_mfma_result_read_too_early():
     assert _seq(mfma, "v_mfma_f32_16x16x32_bf16 v[20:23], v[10:13], a[4:7], v[20:23]", "s_endpgm")
 
 
+def test_checker_uses_the_longer_waits_of_32x32_mfmas():
+    mfma = "v_mfma_f32_32x32x16_bf16 v[10:25], v[2:5], a[0:3], v[10:25]"
+    # 11 wait states cover a 16x16x32 MFMA but not a 32x32x16 one
+    assert _seq(mfma, "s_nop 7", "s_nop 2", "v_max_f32_e32 v1, v20, v11", "s_endpgm")
+    assert not _seq(mfma, "s_nop 7", "s_nop 3", "v_max_f32_e32 v1, v20, v11", "s_endpgm")
+    assert _seq(mfma, "s_nop 7", "s_nop 2", "v_mfma_f32_32x32x16_bf16 v[30:45], v[10:13], a[0:3], 0", "s_endpgm")
+    # the C-operand read lasts longer too
+    war = "v_mfma_f32_32x32x16_bf16 v[30:45], v[2:5], a[0:3], v[10:25]"
+    assert _seq(war, "s_nop 7", "v_mov_b32_e32 v12, 0", "s_endpgm")
+    assert not _seq(war, "s_nop 7", "s_nop 2", "v_mov_b32_e32 v12, 0", "s_endpgm")
+
+
+def test_checker_reads_past_early_exits():
+    # a kernel body does not end at its first s_endpgm
+    text = "\n".join([
+        "\t.type\tk,@function", "k:", "\ts_cbranch_scc1 .LBB0_2", "\ts_endpgm", ".LBB0_2:",
+        "\tv_mfma_f32_32x32x16_bf16 v[10:25], v[2:5], a[0:3], v[10:25]", "\tv_max_f32_e32 v1, v10, v11",
+        "\ts_endpgm", ".Lfunc_end0:"])
+    body = H.kernels(text)["k"]
+    assert H.check(H.parse(body))
+
+
 def test_checker_flags_valu_write_then_mfma_read():
     assert _seq("v_mov_b32_e32 v3, 0", "v_mfma_f32_16x16x32_bf16 v[10:13], v[2:5], a[0:3], 0", "s_endpgm")
     assert _seq("v_accvgpr_write_b32 a2, v7", "v_mfma_f32_16x16x32_bf16 v[10:13], v[2:5], a[0:3], 0", "s_endpgm")
