@@ -16,8 +16,9 @@
 //     prefix row is gathered through the request's slot-table row, a new
 //     token's row read from k_new / v_new) into a four-stage ring, two tiles
 //     of lead.  The slot indices travel by copy four tiles ahead into their
-//     own ring and are read into registers a tile before use.  Rows use the
-//     ra_kv_swz piece layout (conflict-free operand reads).
+//     own ring and are read into registers a tile before use.  A tile is
+//     row-major (a key's D values contiguous, 16-byte slots swizzled by
+//     ext_swz), so one copy instruction moves whole rows.
 //   * The loop runs over 32-key halves, software pipelined in one issue
 //     order that sched_barrier fences hold: the S^T = K Q^T MFMAs of the next
 //     half, each followed by one probability of the current half (fma +
@@ -52,6 +53,8 @@
 namespace {
 
 constexpr int kStages = 4;   // K/V tiles resident in LDS
+template <int V>
+using ic = std::integral_constant<int, V>;
 constexpr int kRing = 4;     // slot-index ring (tiles)
 constexpr int kQB = 2;       // 16-query column blocks per wave (32 query rows)
 // exp2 argument ceiling of the lazy maximum: p <= 2^kLazyLog2
@@ -72,6 +75,26 @@ __device__ __forceinline__ void s_mfma_first(f32x4_t& s, const bf16x8_t& a, cons
 }
 __device__ __forceinline__ void s_mfma_acc(f32x4_t& s, const bf16x8_t& a, const bf16x8_t& qa) {
   asm("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0" : "+v"(s) : "v"(a), "a"(qa));
+}
+
+// Layout of a K or V tile: row-major, row r = RB = 2 D bytes; its 16-byte
+// slot s (head-dimension values 8 s .. 8 s + 7) sits at slot s ^ ext_swz(r).
+// One direct-to-LDS copy instruction (1 KB) then fills 1024 / RB whole rows,
+// each read from one contiguous run of global memory (the 64-byte runs of a
+// piece-group layout touch twice as many cache lines per instruction).  The
+// swizzles were found by an exhaustive search over XOR masks of the row
+// bits against the gfx950 LDS bank model (64 banks of 4 bytes; ds_read_b128
+// in four cycles of the 16-lane groups {0-7, 24-31}, {8-15, 16-23},
+// {32-39, 56-63}, {40-47, 48-55}; ds_read_b64_tr_b16 in two cycles of 32
+// lanes): the K operand reads (rows 8 (c >> 2) + (c & 3) + const, slot
+// 4 ks + (lane >> 4)) and the transposed V reads (rows 8 (lane >> 4) +
+// (c >> 2) + const) then touch 64 distinct banks per cycle.  The masks ignore
+// row bits 2, 4 and 5, which the loops add as constants, so every operand
+// read is one per-lane offset plus an immediate.
+template <int D>
+__device__ __forceinline__ int ext_swz(int r) {
+  if constexpr (D == 128) return ((r & 3) << 1) | (r & 8);
+  else return (r & 2) | ((r & 8) >> 1);
 }
 
 // Requests above this batch size keep the static item order: the ranking
@@ -197,16 +220,21 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void extend_kernel(
   constexpr int kBN = BN;
   constexpr int kBM = 32 * WAVES;             // query rows per work-group
   static_assert(BN == 32 || BN == 64, "tile of one or two 32-key halves");
-  constexpr int KS = D / 32;                  // MFMA k-steps over the head dimension = piece groups
+  constexpr int KS = D / 32;                  // MFMA k-steps over the head dimension
   constexpr int DB = D / 16;                  // 16-row blocks of O^T
-  constexpr int GROUP_B = kBN * 64;           // bytes of one piece group of a tile
-  constexpr int TILE_B = KS * GROUP_B;        // bytes per K (or V) tile
-  constexpr int STAGE_B = 2 * TILE_B;         // K tile then V tile
+  constexpr int RB = 2 * D;                   // bytes of one K (or V) row
+  constexpr int NSL = RB / 16;                // 16-byte slots of a row
+  constexpr int RPI = 1024 / RB;              // rows per 1 KB copy instruction
+  constexpr int TILE_B = kBN * RB;            // bytes per K (or V) tile
+  constexpr int KRING_B = kStages * TILE_B;   // K ring, then the V ring
+  // (a ring position is then an immediate offset of at most 48 KB, within
+  // the 16-bit LDS offset field, once the loops unroll over the stages)
   constexpr int LOADS = TILE_B / (kWaves * 64 * 16);  // DMA instructions per wave per tile per tensor
   constexpr int ROW_STEP = kBN / LOADS;       // a DMA lane covers rows u0 + it * ROW_STEP
   static_assert(LOADS == 1 || LOADS == 2, "index vector width");
-  __shared__ __align__(16) unsigned char kv_lds[kStages * STAGE_B];
-  static_assert((8 * kLptMaxBatch + 8) * 4 <= kStages * STAGE_B, "ranking scratch exceeds the K/V ring");
+  static_assert(LOADS == 1 || RPI * kWaves == ROW_STEP, "a lane's rows are ROW_STEP apart");
+  __shared__ __align__(16) unsigned char kv_lds[2 * KRING_B];
+  static_assert((8 * kLptMaxBatch + 8) * 4 <= 2 * KRING_B, "ranking scratch exceeds the K/V rings");
   // one index copy moves 64 words (rows beyond the tile are never read)
   __shared__ __align__(16) int32_t idx_lds[kRing][64];
 
@@ -267,18 +295,19 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void extend_kernel(
   const int g4 = lane >> 4;
 
   // ---- DMA lane mapping (fixed for the kernel) ----------------------------
-  // instruction ch = it * kWaves + wave covers row block rb = ch / KS, group pg = ch % KS
+  // Instruction ch = it * kWaves + wave fills rows RPI ch .. RPI ch + RPI - 1
+  // (1 KB at ch * 1024): lane l lands in slot l % NSL of row RPI ch + l / NSL
+  // and so carries that row's logical slot (l % NSL) ^ ext_swz(row).
   int dma_row[LOADS];
   uint32_t dma_lds[LOADS];   // byte offset inside a tile (uniform per wave)
   uint32_t dma_gofs[LOADS];  // byte offset inside the gathered global row
 #pragma unroll
   for (int it = 0; it < LOADS; ++it) {
     const int ch = it * kWaves + wave;
-    const int rb = ch / KS, pg = ch % KS;
-    const int u = 16 * rb + (lane >> 2);
+    const int u = RPI * ch + lane / NSL;
     dma_row[it] = u;
-    dma_lds[it] = pg * GROUP_B + rb * 1024;
-    dma_gofs[it] = static_cast<uint32_t>(g * D * 2 + 16 * (4 * pg + ((lane & 3) ^ ra_kv_swz(u))));
+    dma_lds[it] = ch * 1024;
+    dma_gofs[it] = static_cast<uint32_t>(g * D * 2 + 16 * ((lane % NSL) ^ ext_swz<D>(u)));
   }
   const uint32_t row_bytes = static_cast<uint32_t>(hkv) * D * 2;
   const unsigned char* kpool_b = reinterpret_cast<const unsigned char*>(k_pool);
@@ -317,7 +346,7 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void extend_kernel(
       sl[0] = w[0];
     }
   };
-  // Copies of one tile's K and V rows into stage tile % kStages: 2 * LOADS
+  // Copies of one tile's K and V rows into ring stage tile % kStages: 2 * LOADS
   // per wave (source address per lane, LDS base per wave), K then V for each
   // it.  sl = the tile's slot indices (read_idx).  A tile past the last one
   // gets dummy copies of slot 0's row (one cache line per copy) into its
@@ -329,11 +358,11 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void extend_kernel(
   };
   auto prep_kv = [&](int tile, const int32_t (&sl)[LOADS], KvCopies& cp) {
     const int kb = tile * kBN;
-    const uint32_t kst = lds_kv0 + (tile % kStages) * STAGE_B;
+    const uint32_t kst = lds_kv0 + (tile % kStages) * TILE_B;
 #pragma unroll
     for (int it = 0; it < LOADS; ++it) {
       cp.lds[2 * it] = kst + dma_lds[it];
-      cp.lds[2 * it + 1] = kst + TILE_B + dma_lds[it];
+      cp.lds[2 * it + 1] = kst + KRING_B + dma_lds[it];
     }
     if (tile >= n_tiles) {
 #pragma unroll
@@ -450,24 +479,27 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void extend_kernel(
   // row group g4 then holds keys 8 g4 .. 8 g4 + 7 of the half, P^T's
   // B-operand k slots in natural order.
   const int r0 = 8 * (c >> 2) + (c & 3);
-  const uint32_t koff = r0 * 64 + 16 * (g4 ^ ra_kv_swz(r0));
+  uint32_t koff[KS];  // per k-step: row r0, logical slot 4 ks + g4
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) koff[ks] = r0 * RB + 16 * ((4 * ks + g4) ^ ext_swz<D>(r0));
   // V^T via transposed reads: lane supplies row 32 k2 + 4 h + (8 g4 + (c >> 2))
   // and logical piece 2 db + ((c & 3) >> 1), half (c & 1).
   const int vr = 8 * g4 + (c >> 2);
-  uint32_t voff[2];
+  uint32_t voff[DB];  // per 16-row block db of O^T: row vr, logical slot 2 db + ((c & 3) >> 1)
 #pragma unroll
-  for (int e = 0; e < 2; ++e) voff[e] = vr * 64 + 16 * ((2 * e + ((c & 3) >> 1)) ^ ra_kv_swz(vr)) + 8 * (c & 1);
+  for (int db = 0; db < DB; ++db)
+    voff[db] = KRING_B + vr * RB + 16 * ((2 * db + ((c & 3) >> 1)) ^ ext_swz<D>(vr)) + 8 * (c & 1);
 
   // S^T of one 32-key half: s[bb][j], element i = key 32 k2 + 8 g4 + 4 bb + i.
   // (Prologue only; the main loop computes S^T inside the fused step.)
   auto compute_s = [&](f32x4_t (&s)[2][kQB], int tile, int k2) {
-    const unsigned char* kst = kv_lds + (tile % kStages) * STAGE_B;
+    const unsigned char* kst = kv_lds + (tile % kStages) * TILE_B;
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
       for (int bb = 0; bb < 2; ++bb) {
         const bf16x8_t a = __builtin_bit_cast(
-            bf16x8_t, *reinterpret_cast<const uint4*>(kst + koff + ks * GROUP_B + (32 * k2 + 4 * bb) * 64));
+            bf16x8_t, *reinterpret_cast<const uint4*>(kst + koff[ks] + (32 * k2 + 4 * bb) * RB));
 #pragma unroll
         for (int j = 0; j < kQB; ++j) {
           if (ks == 0) s_mfma_first(s[bb][j], a, qT[j][ks]);
@@ -556,18 +588,21 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void extend_kernel(
   // sn, (tile_f, k2_f), when pf is set (its tile is resident by then).
   constexpr int KP = KS > 1 ? 2 : 1;  // k-steps prefetched across steps
   // with_copies: issue the copies prepared by the last tile_top, one every
-  // DB / (2 LOADS) PV steps.
-  auto fused = [&](auto has_next, auto with_copies, f32x4_t (&sn)[2][kQB], int tile_n, int k2_n,
-                   f32x4_t (&sc)[2][kQB], int tile_c, int k2_c, float (&mt)[kQB], bf16x8_t (&kpre)[KP][2], bool pf,
-                   int tile_f, int k2_f) {
+  // DB / (2 LOADS) PV steps.  The ring stages of the halves (sk_n: K of sn,
+  // sv_c: V of sc, sk_f: K of the half after sn) come as compile-time
+  // constants in the steady loops, so every operand read is a per-lane
+  // offset plus an immediate.
+  auto fused = [&](auto has_next, auto with_copies, f32x4_t (&sn)[2][kQB], auto sk_n, int k2_n,
+                   f32x4_t (&sc)[2][kQB], auto sv_c, int k2_c, float (&mt)[kQB], bf16x8_t (&kpre)[KP][2], bool pf,
+                   auto sk_f, int k2_f) {
     constexpr bool HAS_NEXT = decltype(has_next)::value;
     constexpr bool COPIES = decltype(with_copies)::value;
     constexpr int CSTEP = DB / (2 * LOADS) > 0 ? DB / (2 * LOADS) : 1;
     constexpr int NS = 2 * KS * kQB;  // S^T MFMAs of one half
     constexpr int NP = 8 * kQB;       // probabilities per lane per half
     constexpr int VA = 3;             // V^T operands (16-row blocks) read ahead of their PV step
-    const unsigned char* kst = kv_lds + (tile_n % kStages) * STAGE_B + koff + 32 * k2_n * 64;
-    const unsigned char* vst = kv_lds + (tile_c % kStages) * STAGE_B + TILE_B + 32 * k2_c * 64;
+    const unsigned char* kst = kv_lds + static_cast<int>(sk_n) * TILE_B + 32 * k2_n * RB;
+    const unsigned char* vst = kv_lds + static_cast<int>(sv_c) * TILE_B + 32 * k2_c * RB;
     bf16x8_t kf[KS][2];
     bf16x4_t vf[DB][2];
     float p[NP];
@@ -575,15 +610,14 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void extend_kernel(
     auto read_k = [&](int ks) {
 #pragma unroll
       for (int bb = 0; bb < 2; ++bb)
-        kf[ks][bb] = __builtin_bit_cast(bf16x8_t,
-                                        *reinterpret_cast<const uint4*>(kst + ks * GROUP_B + 4 * bb * 64));
+        kf[ks][bb] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const uint4*>(kst + koff[ks] + 4 * bb * RB));
     };
     auto read_v = [&](int db) {
-      const unsigned char* vb = vst + voff[db & 1] + (db >> 1) * GROUP_B;
+      const unsigned char* vb = vst + voff[db];
 #pragma unroll
       for (int h = 0; h < 2; ++h)
         vf[db][h] =
-            __builtin_amdgcn_ds_read_tr16_b64_v4bf16((__attribute__((address_space(3))) bf16x4_t*)(vb + h * 4 * 64));
+            __builtin_amdgcn_ds_read_tr16_b64_v4bf16((__attribute__((address_space(3))) bf16x4_t*)(vb + h * 4 * RB));
     };
     auto prob = [&](int v) {  // v = 8 j + 4 bb + i
       const int j = v >> 3, bb = (v >> 2) & 1, i = v & 3;
@@ -667,13 +701,13 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void extend_kernel(
       for (int i = DB / CSTEP; i < 2 * LOADS; ++i) issue_copy(cp, i);
     }
     if (pf) {
-      const unsigned char* kf_st = kv_lds + (tile_f % kStages) * STAGE_B + koff + 32 * k2_f * 64;
+      const unsigned char* kf_st = kv_lds + static_cast<int>(sk_f) * TILE_B + 32 * k2_f * RB;
 #pragma unroll
       for (int ks = 0; ks < KP; ++ks)
 #pragma unroll
         for (int bb = 0; bb < 2; ++bb)
-          kpre[ks][bb] = __builtin_bit_cast(bf16x8_t,
-                                            *reinterpret_cast<const uint4*>(kf_st + ks * GROUP_B + 4 * bb * 64));
+          kpre[ks][bb] =
+              __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const uint4*>(kf_st + koff[ks] + 4 * bb * RB));
     }
     if constexpr (HAS_NEXT) {
       if constexpr (DB - 2 < kQB) {
@@ -713,54 +747,66 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void extend_kernel(
 #pragma unroll
   for (int j = 0; j < kQB; ++j) mt[j] = half_max(sa, j);
   // K operands of the first two k-steps of a half, read ahead of its step
-  auto load_kpre = [&](int tile, int k2) {
-    const unsigned char* kf_st = kv_lds + (tile % kStages) * STAGE_B + koff + 32 * k2 * 64;
+  auto load_kpre = [&](auto stage, int k2) {
+    const unsigned char* kf_st = kv_lds + static_cast<int>(stage) * TILE_B + 32 * k2 * RB;
 #pragma unroll
     for (int ks = 0; ks < KP; ++ks)
 #pragma unroll
       for (int bb = 0; bb < 2; ++bb)
-        kpre[ks][bb] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const uint4*>(kf_st + ks * GROUP_B + 4 * bb * 64));
+        kpre[ks][bb] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const uint4*>(kf_st + koff[ks] + 4 * bb * RB));
   };
-  if constexpr (BN == 64) load_kpre(0, 1);
+  if constexpr (BN == 64) load_kpre(ic<0>{}, 1);
   pre(sa, 0, 0, mt);
   // The last tile is peeled off the loop so that no branch inside it has two
   // sides computing the same probabilities (the compiler would hoist them out
   // of the fused step).
   if constexpr (BN == 64) {
+    // one tile per call; the tile's ring stage J = t % kStages is a constant
     int t = 0;
-    for (; t + 1 < n_tiles; ++t) {
+    auto tile_body = [&](auto J) -> bool {
+      constexpr int j = decltype(J)::value, j1 = (j + 1) % kStages;
+      if (t + 1 >= n_tiles) return false;
       tile_top(t + 1);
-      fused(yes{}, yes{}, sb, t, 1, sa, t, 0, mt, kpre, true, t + 1, 0);
+      fused(yes{}, yes{}, sb, ic<j>{}, 1, sa, ic<j>{}, 0, mt, kpre, true, ic<j1>{}, 0);
       pre(sb, t, 1, mt);
-      fused(yes{}, no{}, sa, t + 1, 0, sb, t, 1, mt, kpre, true, t + 1, 1);
+      fused(yes{}, no{}, sa, ic<j1>{}, 0, sb, ic<j>{}, 1, mt, kpre, true, ic<j1>{}, 1);
       pre(sa, t + 1, 0, mt);
+      ++t;
+      return true;
+    };
+    while (tile_body(ic<0>{}) && tile_body(ic<1>{}) && tile_body(ic<2>{}) && tile_body(ic<3>{})) {
     }
-    fused(yes{}, no{}, sb, t, 1, sa, t, 0, mt, kpre, false, 0, 0);
+    const int ts = t % kStages;
+    fused(yes{}, no{}, sb, ts, 1, sa, ts, 0, mt, kpre, false, 0, 0);
     pre(sb, t, 1, mt);
-    fused(no{}, no{}, sa, 0, 0, sb, t, 1, mt, kpre, false, 0, 0);
+    fused(no{}, no{}, sa, 0, 0, sb, ts, 1, mt, kpre, false, 0, 0);
   } else {
     // One half per tile: the step of tile t + 1 follows that tile's barrier
     // (its K operands are read there); two tiles per iteration so the S^T
-    // buffers alternate without copies.
+    // buffers alternate without copies.  (The ring stages stay runtime
+    // values here: unrolled over them, this shape's register allocation
+    // moves accumulators next to the inline-assembly MFMAs.)
     int t = 0;
     for (; t + 2 < n_tiles; t += 2) {
+      const int s0 = t % kStages, s1 = (t + 1) % kStages, s2 = (t + 2) % kStages;
       tile_top(t + 1);
-      load_kpre(t + 1, 0);
-      fused(yes{}, yes{}, sb, t + 1, 0, sa, t, 0, mt, kpre, false, 0, 0);
+      load_kpre(s1, 0);
+      fused(yes{}, yes{}, sb, s1, 0, sa, s0, 0, mt, kpre, false, 0, 0);
       pre(sb, t + 1, 0, mt);
       tile_top(t + 2);
-      load_kpre(t + 2, 0);
-      fused(yes{}, yes{}, sa, t + 2, 0, sb, t + 1, 0, mt, kpre, false, 0, 0);
+      load_kpre(s2, 0);
+      fused(yes{}, yes{}, sa, s2, 0, sb, s1, 0, mt, kpre, false, 0, 0);
       pre(sa, t + 2, 0, mt);
     }
+    const int ts = t % kStages, ts1 = (t + 1) % kStages;
     if (t + 1 < n_tiles) {
       tile_top(t + 1);
-      load_kpre(t + 1, 0);
-      fused(yes{}, yes{}, sb, t + 1, 0, sa, t, 0, mt, kpre, false, 0, 0);
+      load_kpre(ts1, 0);
+      fused(yes{}, yes{}, sb, ts1, 0, sa, ts, 0, mt, kpre, false, 0, 0);
       pre(sb, t + 1, 0, mt);
-      fused(no{}, no{}, sa, 0, 0, sb, t + 1, 0, mt, kpre, false, 0, 0);
+      fused(no{}, no{}, sa, 0, 0, sb, ts1, 0, mt, kpre, false, 0, 0);
     } else {
-      fused(no{}, no{}, sb, 0, 0, sa, t, 0, mt, kpre, false, 0, 0);
+      fused(no{}, no{}, sb, 0, 0, sa, ts, 0, mt, kpre, false, 0, 0);
     }
   }
 
