@@ -257,13 +257,20 @@ def main():
     out_d = torch.empty_like(inp.q_dec) if inp.n_dec else None
 
     ws_t = workspace if ws_bytes else None
+    # A batch without decodes takes the extend entry point with key splits
+    # (the library picks them; none when the work items already fill the chip).
+    ext_ws_bytes = run.extend_workspace_bytes(inp, 0) if inp.n_ext else 0
+    ext_ws = torch.empty(ext_ws_bytes, dtype=torch.uint8, device="cuda") if ext_ws_bytes else None
+    ext_splits = 0 if inp.n_dec == 0 else None
+    ext_ns = pa.ra_extend_num_splits(inp.n_ext, inp.max_extend_len, sc.hq, sc.hkv, 0) if ext_splits == 0 else 1
+    log(f"[bench] extend key splits: {ext_ns}")
     flush_buf = torch.empty(FLUSH_BYTES, dtype=torch.uint8, device="cuda")
 
     def step():
         """One pass of the hot path: store new K/V, then the mixed batch call."""
         if n_new:
             pa.ra_store_kv(inp.new_slots, inp.k_new, inp.v_new, run.k_pool, run.v_pool)
-        run.mixed(inp, workspace=ws_t, out_ext=out_e, out_dec=out_d)
+        run.mixed(inp, workspace=ws_t, out_ext=out_e, out_dec=out_d, ext_splits=ext_splits, ext_workspace=ext_ws)
 
     def step_sequential(ev):
         """The same work with each kernel timed alone (for the rooflines)."""
@@ -272,7 +279,7 @@ def main():
             pa.ra_store_kv(inp.new_slots, inp.k_new, inp.v_new, run.k_pool, run.v_pool)
         ev[1].record(stream)
         if inp.n_ext:
-            run.extend(inp, out=out_e)
+            run.extend(inp, out=out_e, num_splits=ext_splits, workspace=ext_ws)
         ev[2].record(stream)
         if inp.n_dec:
             run.decode(inp, workspace=ws_t, out=out_d)
@@ -388,7 +395,8 @@ def main():
                    "pool_slots": sc.pool_slots, "extend_requests": inp.n_ext, "decode_requests": inp.n_dec,
                    "sum_extend_tokens": inp.total_ext, "sum_decode_context": work["sum_l"],
                    "history_requests": sc.history_len, "tree_calls": run.history_ops,
-                   "hit_rate": inp.plan.hit_rate, "parallelism": "none (1 GPU)"},
+                   "hit_rate": inp.plan.hit_rate, "extend_key_splits": ext_ns if inp.n_ext else None,
+                   "parallelism": "none (1 GPU)"},
         "clock_warmup": {"seconds": args.clock_warmup, "steps": clock_steps},
         "ms_per_step_sequential_cold": ms_seq,
         "roofline": roof,

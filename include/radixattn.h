@@ -191,6 +191,31 @@ int ra_extend_attention(const void* q, const void* k_new, const void* v_new, int
                         int32_t max_extend_len, int32_t hq, int32_t hkv, int32_t d, float scale,
                         void* out, hipStream_t stream);
 
+/* Extend attention with key splits, for batches whose work items would not
+ * fill the chip (few requests or a head shard; the same operation as
+ * ra_extend_attention, section 3 and Appendix A.1).  Each item's keys are cut
+ * into runs of whole tiles processed in parallel; each run writes its rows'
+ * output normalised over its keys (fp32) and their log-sum-exp to
+ * `workspace`, and a second kernel merges them.  num_splits = 0 picks the
+ * count (1 when the items already fill the chip); num_splits > 0 asks for
+ * that many (at most 16; items too short for them use fewer).  workspace
+ * (16-byte aligned, owned by the caller, contents undefined on return) must
+ * hold ra_extend_workspace_bytes(...) bytes for the same arguments, which is
+ * 0 when the call does not split: then workspace may be NULL.  Other arguments,
+ * layouts and bounds as ra_extend_attention; RA_EINVAL for a negative
+ * num_splits or a short workspace. */
+int32_t ra_extend_num_splits(int32_t batch, int32_t max_extend_len, int32_t hq, int32_t hkv, int32_t num_splits);
+size_t ra_extend_workspace_bytes(int64_t total_tokens, int32_t batch, int32_t max_extend_len, int32_t hq,
+                                 int32_t hkv, int32_t d, int32_t num_splits);
+int ra_extend_attention_split(const void* q, const void* k_new, const void* v_new, int64_t total_tokens,
+                              const void* k_pool, const void* v_pool, int64_t pool_slots,
+                              const int32_t* req_to_token, int64_t rtt_rows, int64_t rtt_stride,
+                              const int32_t* req_pool_idx, const int32_t* prefix_lens,
+                              const int32_t* extend_lens, const int32_t* extend_start, int32_t batch,
+                              int32_t max_extend_len, int32_t hq, int32_t hkv, int32_t d, float scale,
+                              int32_t num_splits, void* workspace, size_t workspace_bytes, void* out,
+                              hipStream_t stream);
+
 /* Decode attention: query r ([B, Hq, D] bf16) at position L_r - 1 over
  * positions 0 .. L_r - 1 (its own K/V already stored), seq_lens = L_r >= 1.
  * Long contexts are cut into KV chunks processed in parallel; each chunk

@@ -56,6 +56,11 @@ _SIGS = {
     "ra_store_kv": ([_vp, _vp, _vp, _i64, _vp, _vp, _i64, _i32, _i32, _vp], ctypes.c_int),
     "ra_extend_attention": ([_vp, _vp, _vp, _i64, _vp, _vp, _i64, _vp, _i64, _i64, _vp, _vp, _vp, _vp,
                              _i32, _i32, _i32, _i32, _i32, ctypes.c_float, _vp, _vp], ctypes.c_int),
+    "ra_extend_num_splits": ([_i32, _i32, _i32, _i32, _i32], _i32),
+    "ra_extend_workspace_bytes": ([_i64, _i32, _i32, _i32, _i32, _i32, _i32], ctypes.c_size_t),
+    "ra_extend_attention_split": ([_vp, _vp, _vp, _i64, _vp, _vp, _i64, _vp, _i64, _i64, _vp, _vp, _vp, _vp,
+                                   _i32, _i32, _i32, _i32, _i32, ctypes.c_float, _i32, _vp, ctypes.c_size_t, _vp,
+                                   _vp], ctypes.c_int),
     "ra_decode_workspace_bytes": ([_i32, _i32, _i32, _i32, _i32, _i32], ctypes.c_size_t),
     "ra_decode_chunk_len": ([_i32, _i32, _i32, _i32], _i32),
     "ra_decode_attention": ([_vp, _vp, _vp, _i64, _vp, _i64, _i64, _vp, _vp, _i32, _i32, _i32, _i32, _i32,
@@ -295,6 +300,41 @@ def ra_extend_attention(q, k_new, v_new, k_pool, v_pool, req_to_token, req_pool_
         _dev(extend_lens, torch.int32, "extend_lens"), _dev(extend_start, torch.int32, "extend_start"),
         prefix_lens.shape[0], int(max_extend_len), hq, hkv, d, float(scale), _dev(out, torch.bfloat16, "out"),
         _stream(stream)))
+    return out
+
+
+def ra_extend_num_splits(batch: int, max_extend_len: int, hq: int, hkv: int, num_splits: int = 0) -> int:
+    return int(_lib.ra_extend_num_splits(batch, max_extend_len, hq, hkv, num_splits))
+
+
+def ra_extend_workspace_bytes(total_tokens: int, batch: int, max_extend_len: int, hq: int, hkv: int, d: int,
+                              num_splits: int = 0) -> int:
+    return int(_lib.ra_extend_workspace_bytes(total_tokens, batch, max_extend_len, hq, hkv, d, num_splits))
+
+
+def ra_extend_attention_split(q, k_new, v_new, k_pool, v_pool, req_to_token, req_pool_idx, prefix_lens, extend_lens,
+                              extend_start, max_extend_len: int, scale: float, num_splits: int = 0, workspace=None,
+                              out=None, stream=None):
+    import torch
+
+    total, hq, d = q.shape
+    hkv = k_new.shape[1]
+    batch = prefix_lens.shape[0]
+    need = ra_extend_workspace_bytes(total, batch, int(max_extend_len), hq, hkv, d, num_splits)
+    if workspace is None and need:
+        workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
+    if out is None:
+        out = torch.empty_like(q)
+    ws_ptr = _dev(workspace, None, "workspace") if workspace is not None else None
+    ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    _check(_lib.ra_extend_attention_split(
+        _dev(q, torch.bfloat16, "q"), _dev(k_new, torch.bfloat16, "k_new"), _dev(v_new, torch.bfloat16, "v_new"),
+        total, _dev(k_pool, torch.bfloat16, "k_pool"), _dev(v_pool, torch.bfloat16, "v_pool"), k_pool.shape[0],
+        _dev(req_to_token, torch.int32, "req_to_token"), req_to_token.shape[0], req_to_token.shape[1],
+        _dev(req_pool_idx, torch.int32, "req_pool_idx"), _dev(prefix_lens, torch.int32, "prefix_lens"),
+        _dev(extend_lens, torch.int32, "extend_lens"), _dev(extend_start, torch.int32, "extend_start"),
+        batch, int(max_extend_len), hq, hkv, d, float(scale), int(num_splits), ws_ptr, ws_bytes,
+        _dev(out, torch.bfloat16, "out"), _stream(stream)))
     return out
 
 

@@ -44,6 +44,7 @@
 //     sums come from an MFMA against a ones operand, so numerator and
 //     denominator see the same bf16 P.
 
+#include <algorithm>
 #include <atomic>
 #include <type_traits>
 
@@ -97,6 +98,12 @@ __device__ __forceinline__ int ext_swz(int r) {
   else return (r & 2) | ((r & 8) >> 1);
 }
 
+// Key splits: an item whose keys are cut into splits takes at least this many
+// tiles per split (fewer splits for shorter items; the rest stay empty), and
+// at most kMaxSplits splits.
+constexpr int kMinSplitTiles = 8;
+constexpr int kMaxSplits = 16;
+
 // Requests above this batch size keep the static item order: the ranking
 // below is quadratic in the batch, and its scratch (8 * batch + 8 words)
 // lives in the K/V ring, whose smallest configuration (D = 64, 128 rows) has
@@ -104,9 +111,9 @@ __device__ __forceinline__ int ext_swz(int r) {
 constexpr int kLptMaxBatch = 1016;
 
 // Work item of block k in longest-first order.  A unit is (request, query
-// tile).  Units are ordered by their request's key count P + E, longest
-// first (ties by request index), and within a request by query tile, the
-// last (longest) tile first.  Block k takes unit k / hkv of kv head
+// tile, key split).  Units are ordered by their request's key count P + E,
+// longest first (ties by request index), and within a request by query tile,
+// the last (longest) tile first, then by split.  Block k takes unit k / hkv of kv head
 // k % hkv.  The dispatcher starts blocks in index order and deals them to
 // the XCDs round-robin, so every XCD runs its share longest-first, and with
 // 8 | hkv each XCD keeps whole kv heads (its L2 sees their rows only).  A
@@ -121,8 +128,8 @@ template <bool UNIFORM>
 __device__ bool ra_lpt_item(int32_t* scratch, int64_t k, int32_t hkv, int32_t batch, int32_t tpb,
                             const int32_t* __restrict__ req_pool_idx, const int32_t* __restrict__ prefix_lens,
                             const int32_t* __restrict__ extend_lens, const int32_t* __restrict__ extend_start,
-                            int64_t total_tokens, int64_t rtt_stride, int& g, int& b, int& qt,
-                            int32_t (&req_args)[4], int nthreads) {
+                            int64_t total_tokens, int64_t rtt_stride, int32_t nsplit, int& g, int& b, int& qt,
+                            int& sp, int32_t (&req_args)[4], int nthreads) {
   const int bp = (batch + 3) & ~3;         // batch padded to whole int4 reads
   int32_t* args = scratch;                 // [batch][4] start, E, P, table row as passed (16-byte entries)
   int32_t* cost = scratch + 4 * batch;     // [bp] key count of the request's units, -1 if none, -2 padding
@@ -142,7 +149,7 @@ __device__ bool ra_lpt_item(int32_t* scratch, int64_t k, int32_t hkv, int32_t ba
     *reinterpret_cast<int4*>(&args[4 * t]) = make_int4(st, el, pl, rp);
     const int64_t e = (st < 0 || st > total_tokens) ? 0 : min<int64_t>(el, total_tokens - st);
     const int64_t p = min<int64_t>(max(pl, 0), rtt_stride);
-    const int64_t nu = e > 0 ? (e + tpb - 1) / tpb : 0;
+    const int64_t nu = e > 0 ? (e + tpb - 1) / tpb * nsplit : 0;
     nun[t] = static_cast<int32_t>(nu);
     cost[t] = nu > 0 ? static_cast<int32_t>(min<int64_t>(p + e, INT32_MAX)) : -1;
   }
@@ -200,7 +207,8 @@ __device__ bool ra_lpt_item(int32_t* scratch, int64_t k, int32_t hkv, int32_t ba
   if (req < 0) return false;
   g = static_cast<int>(k % hkv);
   b = req;
-  qt = tile;
+  qt = tile / nsplit;
+  sp = tile % nsplit;
   return true;
 }
 
@@ -208,6 +216,12 @@ __device__ bool ra_lpt_item(int32_t* scratch, int64_t k, int32_t hkv, int32_t ba
 // two 32-key halves per tile; 32: one).  <D, 8, 64>: 256 rows, one
 // work-group per CU; <D, 4, 32>: 128 rows, two work-groups per CU (65 KB of
 // LDS each).  Either way two waves share each SIMD.
+// nsplit > 1: the keys of each (request, kv head, query tile) are cut into
+// up to nsplit runs of whole tiles, one work item each; an item writes its
+// rows' output normalised over its own keys (fp32, ws_o [nsplit][rows][D],
+// row = token * Hq + head) and their log2-sum-exp of scaled scores (ws_lse
+// [nsplit][rows], -inf where the item saw no key of the row), and
+// extend_combine_kernel merges them.
 template <int D, int WAVES, int BN>
 __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void extend_kernel(
     const __bf16* __restrict__ q, const __bf16* __restrict__ k_new, const __bf16* __restrict__ v_new,
@@ -215,7 +229,8 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void extend_kernel(
     int64_t pool_slots, const int32_t* __restrict__ rtt, int64_t rtt_rows, int64_t rtt_stride,
     const int32_t* __restrict__ req_pool_idx, const int32_t* __restrict__ prefix_lens,
     const int32_t* __restrict__ extend_lens, const int32_t* __restrict__ extend_start, int32_t batch,
-    int32_t hkv, int32_t grp, int32_t n_qtiles, int32_t lpt, float scale_log2, __bf16* __restrict__ out) {
+    int32_t hkv, int32_t grp, int32_t n_qtiles, int32_t lpt, float scale_log2, int32_t nsplit,
+    float* __restrict__ ws_o, float* __restrict__ ws_lse, __bf16* __restrict__ out) {
   constexpr int kWaves = WAVES;
   constexpr int kBN = BN;
   constexpr int kBM = 32 * WAVES;             // query rows per work-group
@@ -252,23 +267,26 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void extend_kernel(
   constexpr bool kUniform = WAVES == 8;
   const int64_t blk = kUniform ? static_cast<int64_t>(__builtin_amdgcn_workgroup_id_x()) : blockIdx.x;
   const int tpb = kBM / grp;  // new tokens per tile
-  const int64_t n_items = static_cast<int64_t>(hkv) * batch * n_qtiles;
-  int g, b, qt;
+  const int64_t n_items = static_cast<int64_t>(hkv) * batch * n_qtiles * nsplit;
+  int g, b, qt, sp;
   int32_t req_args[4];  // extend_start, extend_lens, prefix_lens, req_pool_idx of request b
   if (lpt) {
     if (!ra_lpt_item<kUniform>(reinterpret_cast<int32_t*>(kv_lds), blk, hkv, batch, tpb, req_pool_idx, prefix_lens,
-                     extend_lens, extend_start, total_tokens, rtt_stride, g, b, qt, req_args, WAVES * 64))
+                     extend_lens, extend_start, total_tokens, rtt_stride, nsplit, g, b, qt, sp, req_args, WAVES * 64))
       return;
   } else {
     // Static order: XCD i % 8 takes a contiguous eighth of the (kv head,
-    // request, query tile) order.
+    // request, query tile, split) order.
     const int64_t per_xcd = (n_items + 7) / 8;
     const int64_t item = (blk % 8) * per_xcd + blk / 8;
     if (item >= n_items) return;
-    g = static_cast<int>(item / (static_cast<int64_t>(batch) * n_qtiles));
-    const int rem = static_cast<int>(item % (static_cast<int64_t>(batch) * n_qtiles));
-    b = rem / n_qtiles;
-    qt = n_qtiles - 1 - rem % n_qtiles;
+    const int64_t per_head = static_cast<int64_t>(batch) * n_qtiles * nsplit;
+    g = static_cast<int>(item / per_head);
+    const int64_t rem = item % per_head;
+    b = static_cast<int>(rem / (static_cast<int64_t>(n_qtiles) * nsplit));
+    const int rq = static_cast<int>(rem % (static_cast<int64_t>(n_qtiles) * nsplit));
+    qt = n_qtiles - 1 - rq / nsplit;
+    sp = rq % nsplit;
     req_args[0] = extend_start[b], req_args[1] = extend_lens[b], req_args[2] = prefix_lens[b];
     req_args[3] = req_pool_idx[b];
   }
@@ -286,7 +304,16 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void extend_kernel(
   const int32_t* trow = rtt + rrow * rtt_stride;
   const int kend = P + tok_end;
   const int hq = hkv * grp;
-  const int n_tiles = (kend + kBN - 1) / kBN;
+  // This item's tiles: kt0 is its first key, n_tiles its tile count (all of
+  // the keys unless they are split).
+  const int nt_all = (kend + kBN - 1) / kBN;
+  int t_lo = 0, n_tiles = nt_all;
+  if (nsplit > 1) {
+    const int ns = min(nsplit, max(1, nt_all / kMinSplitTiles));
+    t_lo = sp < ns ? sp * nt_all / ns : 0;
+    n_tiles = sp < ns ? (sp + 1) * nt_all / ns - t_lo : 0;
+  }
+  const int kt0 = t_lo * kBN;
 
   const int tid = static_cast<int>(kUniform ? __builtin_amdgcn_workitem_id_x() : threadIdx.x);
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform (SGPR)
@@ -332,7 +359,7 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void extend_kernel(
   // each wave's count of outstanding loads per tile is fixed.
   auto issue_idx = [&](int tile) {
     if (wave != 0) return;
-    const int pos = tile * kBN + idx_pos;
+    const int pos = kt0 + tile * kBN + idx_pos;
     ra_dma4(trow + (tile < n_tiles && pos < P ? pos : 0), ra_lds_addr(&idx_lds[tile % kRing][0]));
   };
   // This lane's LOADS slot indices of a tile, read from the index ring (one
@@ -357,7 +384,7 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void extend_kernel(
     uint32_t lds[2 * LOADS];
   };
   auto prep_kv = [&](int tile, const int32_t (&sl)[LOADS], KvCopies& cp) {
-    const int kb = tile * kBN;
+    const int kb = kt0 + tile * kBN;
     const uint32_t kst = lds_kv0 + (tile % kStages) * TILE_B;
 #pragma unroll
     for (int it = 0; it < LOADS; ++it) {
@@ -437,6 +464,23 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void extend_kernel(
     qok[j] = it < tok_end;
     qlim[j] = P + min(it, tok_end - 1);
     qrow[j] = (start + min(it, tok_end - 1)) * hq + g * grp + m % grp;
+  }
+  const int64_t ws_row0 = static_cast<int64_t>(sp) * total_tokens * hq;  // this split's rows in the workspace
+  if (n_tiles == 0) {
+    // a split past the end of a short item's keys: its rows saw no key
+    // (zero output, log2-sum-exp -inf, so the merge reads finite values only)
+#pragma unroll
+    for (int j = 0; j < kQB; ++j) {
+      if (!qok[j]) continue;
+      float* wp = ws_o + (ws_row0 + qrow[j]) * D + 4 * g4;
+#pragma unroll
+      for (int db = 0; db < DB; ++db) *reinterpret_cast<float4*>(wp + 16 * db) = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (g4 == 0) ws_lse[ws_row0 + qrow[j]] = -INFINITY;
+    }
+    return;
+  }
+#pragma unroll
+  for (int j = 0; j < kQB; ++j) {
     const __bf16* qp = q + qrow[j] * D + 8 * g4;
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) qT[j][ks] = __builtin_bit_cast(bf16x8_t, ra_ld16(qp + 32 * ks));
@@ -523,7 +567,7 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void extend_kernel(
   // causal mask (diagonal halves only, maxima recomputed), then the rare move
   // of the running maximum with its rescale of O^T.
   auto pre = [&](f32x4_t (&s)[2][kQB], int tile, int k2, float (&mt)[kQB]) {
-    const int kh = tile * kBN + 32 * k2;  // first key of the half
+    const int kh = kt0 + tile * kBN + 32 * k2;  // first key of the half
     if (kh + 31 > P + tok0) {
 #pragma unroll
       for (int j = 0; j < kQB; ++j) {
@@ -825,6 +869,23 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void extend_kernel(
                    : "+a"(o[0][j]), "+a"(o[1][j]), "+a"(o[2][j]), "+a"(o[3][j]), "+a"(o[4][j]));
     }
   }
+  if (nsplit > 1) {
+    // Partial output over this split's keys.  A row whose keys all lie past
+    // its causal limit has a zero sum: zero output, log2-sum-exp -inf.
+#pragma unroll
+    for (int j = 0; j < kQB; ++j) {
+      if (!qok[j]) continue;
+      const float l = o[DB][j][0];
+      const float inv = l > 0.f ? 1.f / l : 0.f;
+      float* wp = ws_o + (ws_row0 + qrow[j]) * D + 4 * g4;
+#pragma unroll
+      for (int db = 0; db < DB; ++db)
+        *reinterpret_cast<float4*>(wp + 16 * db) =
+            make_float4(o[db][j][0] * inv, o[db][j][1] * inv, o[db][j][2] * inv, o[db][j][3] * inv);
+      if (g4 == 0) ws_lse[ws_row0 + qrow[j]] = l > 0.f ? m_run[j] * scale_log2 + __log2f(l) : -INFINITY;
+    }
+    return;
+  }
 #pragma unroll
   for (int j = 0; j < kQB; ++j) {
     if (!qok[j]) continue;
@@ -840,15 +901,103 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void extend_kernel(
   }
 }
 
+// Merges the key splits of every new token's rows: each request's output
+// rows [start, start + E) x Hq x D are one contiguous run, read four values
+// per thread; weights 2^(lse_i - max lse) (0 for a split that saw no key of
+// the row: lse -inf, output zero).  The loads of two splits go out before any
+// is used, so a thread waits for memory once per pair of splits.  max_tok
+// bounds E as the extend kernel's query tiles do.
+template <int D>
+__global__ __launch_bounds__(256) void extend_combine_kernel(const float* __restrict__ ws_o,
+                                                             const float* __restrict__ ws_lse,
+                                                             const int32_t* __restrict__ extend_lens,
+                                                             const int32_t* __restrict__ extend_start,
+                                                             int64_t total_tokens, int32_t max_tok, int32_t hq,
+                                                             int32_t nsplit, __bf16* __restrict__ out) {
+  const int b = blockIdx.x;  // request (the grid's y extent is limited to 65535)
+  const int64_t start = extend_start[b];
+  if (start < 0 || start > total_tokens) return;
+  const int64_t E = min(min<int64_t>(extend_lens[b], total_tokens - start), static_cast<int64_t>(max_tok));
+  const int64_t n4 = E * hq * (D / 4);                 // four-value groups of the request
+  const int64_t rows_total = total_tokens * hq;        // rows per split
+  const int64_t base = start * hq * (D / 4);
+  for (int64_t i = static_cast<int64_t>(blockIdx.y) * 256 + threadIdx.x; i < n4;
+       i += static_cast<int64_t>(gridDim.y) * 256) {
+    const int64_t e = base + i;
+    const int64_t row = e / (D / 4);
+    float m = -INFINITY, wsum = 0.f;  // running maximum of the lse seen, weight sum
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int s0 = 0; s0 < nsplit; s0 += 2) {
+      float l[2];
+      float4 v[2];
+#pragma unroll
+      for (int k = 0; k < 2; ++k) {
+        const int64_t s = min(s0 + k, nsplit - 1);  // an odd count repeats the last split, weighted 0
+        l[k] = ws_lse[s * rows_total + row];
+        v[k] = *reinterpret_cast<const float4*>(ws_o + (s * rows_total) * D + 4 * e);
+      }
+      if (s0 + 1 >= nsplit) l[1] = -INFINITY;
+      const float mn = fmaxf(m, fmaxf(l[0], l[1]));
+      if (mn == -INFINITY) continue;
+      const float a = ra_exp2(m - mn);  // 0 while m = -inf
+      wsum *= a;
+      acc.x *= a, acc.y *= a, acc.z *= a, acc.w *= a;
+#pragma unroll
+      for (int k = 0; k < 2; ++k) {
+        const float w = ra_exp2(l[k] - mn);
+        wsum += w;
+        acc.x += w * v[k].x, acc.y += w * v[k].y, acc.z += w * v[k].z, acc.w += w * v[k].w;
+      }
+      m = mn;
+    }
+    const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
+    uint2 w;
+    w.x = ra_pack_bf16x2(acc.x * inv, acc.y * inv);
+    w.y = ra_pack_bf16x2(acc.z * inv, acc.w * inv);
+    *reinterpret_cast<uint2*>(out + 4 * e) = w;
+  }
+}
+
 template <int D, int WAVES, int BN>
 void launch_wide(int64_t items, hipStream_t stream, const __bf16* qp, const __bf16* knp, const __bf16* vnp,
                  int64_t total_tokens, const __bf16* kp, const __bf16* vp, int64_t pool_slots, const int32_t* rtt,
                  int64_t rtt_rows, int64_t rtt_stride, const int32_t* rpi, const int32_t* pl, const int32_t* el,
                  const int32_t* es, int32_t batch, int32_t hkv, int32_t grp, int32_t n_qtiles, int32_t lpt, float scale_log2,
-                 __bf16* op) {
+                 int32_t nsplit, float* ws_o, float* ws_lse, __bf16* op) {
   hipLaunchKernelGGL((extend_kernel<D, WAVES, BN>), dim3(static_cast<uint32_t>(items)), dim3(WAVES * 64), 0,
                      stream, qp, knp, vnp, total_tokens, kp, vp, pool_slots, rtt, rtt_rows, rtt_stride, rpi, pl, el,
-                     es, batch, hkv, grp, n_qtiles, lpt, scale_log2, op);
+                     es, batch, hkv, grp, n_qtiles, lpt, scale_log2, nsplit, ws_o, ws_lse, op);
+}
+
+// Shape and key splits of a call: 256 or 128 query rows per work-group and
+// the number of key splits per item.
+struct ExtendPlan {
+  int32_t rows;
+  int32_t nsplit;
+};
+
+// num_splits < 0: the entry point without a workspace (no splits).  At least
+// 256 query rows per kv head (new tokens x query heads per kv head) take the
+// 256-row configuration; fewer would leave most of its tile empty, so they
+// take the 128-row one.  Without splits the 128-row one also serves a batch
+// whose 256-row work-groups would not reach one per CU (few requests and few
+// kv heads, e.g. a head shard): twice the work-groups, so more CUs share the
+// work.  With num_splits = 0 such a batch keeps its shape and its items' keys
+// are split until the work-groups fill every work-group slot of the chip
+// once; num_splits > 0 asks for that many splits (at most kMaxSplits).
+ExtendPlan extend_plan(int32_t batch, int32_t max_extend_len, int32_t grp, int32_t hkv, int32_t num_splits) {
+  ExtendPlan pl{static_cast<int64_t>(max_extend_len) * grp >= 256 ? 256 : 128, 1};
+  const int32_t tpb = pl.rows / grp;
+  const int64_t items = static_cast<int64_t>(batch) * hkv * ((static_cast<int64_t>(max_extend_len) + tpb - 1) / tpb);
+  const int64_t slots = static_cast<int64_t>(ra_device_cus()) * (pl.rows == 256 ? 1 : 2);
+  if (num_splits < 0) {
+    if (pl.rows == 256 && items < ra_device_cus()) pl.rows = 128;
+  } else if (num_splits > 0) {
+    pl.nsplit = std::min(num_splits, kMaxSplits);
+  } else if (items > 0 && items < slots) {
+    pl.nsplit = static_cast<int32_t>(std::min<int64_t>(kMaxSplits, (slots + items - 1) / items));
+  }
+  return pl;
 }
 
 }  // namespace
@@ -874,11 +1023,12 @@ static int extend_launch(const void* q, const void* k_new, const void* v_new, in
                           int64_t rtt_rows, int64_t rtt_stride, const int32_t* req_pool_idx,
                           const int32_t* prefix_lens, const int32_t* extend_lens, const int32_t* extend_start,
                           int32_t batch, int32_t max_extend_len, int32_t hq, int32_t hkv, int32_t d, float scale,
-                          void* out, int32_t rows, hipStream_t stream) {
+                          void* out, ExtendPlan plan, void* workspace, hipStream_t stream) {
   const int32_t grp = hq / hkv;
+  const int32_t rows = plan.rows;
   const int32_t tpb = (rows == 256 ? 256 : 128) / grp;
   const int64_t n_qtiles = (static_cast<int64_t>(max_extend_len) + tpb - 1) / tpb;
-  const int64_t items = (static_cast<int64_t>(batch) * hkv * n_qtiles + 7) / 8 * 8;  // whole XCD rounds
+  const int64_t items = (static_cast<int64_t>(batch) * hkv * n_qtiles * plan.nsplit + 7) / 8 * 8;  // whole XCD rounds
   if (items > INT32_MAX) return ra_fail(RA_EINVAL, "ra_extend_attention: too many work items");
   const float scale_log2 = scale * RA_LOG2E;
   auto* qp = static_cast<const __bf16*>(q);
@@ -888,6 +1038,8 @@ static int extend_launch(const void* q, const void* k_new, const void* v_new, in
   auto* vp = static_cast<const __bf16*>(v_pool);
   auto* op = static_cast<__bf16*>(out);
   const int32_t nq = static_cast<int32_t>(n_qtiles);
+  float* ws_o = plan.nsplit > 1 ? static_cast<float*>(workspace) : nullptr;
+  float* ws_lse = plan.nsplit > 1 ? ws_o + static_cast<int64_t>(plan.nsplit) * total_tokens * hq * d : nullptr;
   // Longest first only matters when the work-groups take more than one round
   // of the chip's work-group slots (two per CU with 128 rows, one with 256).
   const int64_t slots = static_cast<int64_t>(ra_device_cus()) * (rows == 256 ? 1 : 2);
@@ -895,7 +1047,7 @@ static int extend_launch(const void* q, const void* k_new, const void* v_new, in
 #define RA_WIDE_LAUNCH(DD, W, B)                                                                                   \
   launch_wide<DD, W, B>(items, stream, qp, knp, vnp, total_tokens, kp, vp, pool_slots, req_to_token, rtt_rows,     \
                         rtt_stride, req_pool_idx, prefix_lens, extend_lens, extend_start, batch, hkv, grp, nq, lpt, \
-                        scale_log2, op)
+                        scale_log2, plan.nsplit, ws_o, ws_lse, op)
   if (rows == 256) {
     if (d == 128) RA_WIDE_LAUNCH(128, 8, 64);
     else RA_WIDE_LAUNCH(64, 8, 64);
@@ -904,7 +1056,18 @@ static int extend_launch(const void* q, const void* k_new, const void* v_new, in
     else RA_WIDE_LAUNCH(64, 4, 32);
   }
 #undef RA_WIDE_LAUNCH
-  return ra_check_launch("ra_extend_attention(fused)");
+  int st = ra_check_launch("ra_extend_attention(fused)");
+  if (st != RA_OK || plan.nsplit <= 1) return st;
+  const int64_t max_tok = n_qtiles * tpb;
+  const int64_t groups = max_tok * hq * d / 4;
+  const dim3 cgrid(static_cast<uint32_t>(batch), static_cast<uint32_t>(std::min<int64_t>((groups + 255) / 256, 1024)));
+  if (d == 128)
+    hipLaunchKernelGGL(extend_combine_kernel<128>, cgrid, dim3(256), 0, stream, ws_o, ws_lse, extend_lens,
+                       extend_start, total_tokens, static_cast<int32_t>(max_tok), hq, plan.nsplit, op);
+  else
+    hipLaunchKernelGGL(extend_combine_kernel<64>, cgrid, dim3(256), 0, stream, ws_o, ws_lse, extend_lens,
+                       extend_start, total_tokens, static_cast<int32_t>(max_tok), hq, plan.nsplit, op);
+  return ra_check_launch("ra_extend_attention(combine)");
 }
 
 // Argument checks shared with ra_mixed_attention: RA_OK when the call may
@@ -947,19 +1110,52 @@ extern "C" int ra_extend_attention(const void* q, const void* k_new, const void*
                                    extend_lens, extend_start, total_tokens, max_extend_len, nullptr, 0, stream);
     if (cst != RA_OK) return cst;
   }
-  const int32_t grp = hq / hkv;
-  // At least 256 query rows per kv head (new tokens x query heads per kv
-  // head): the 256-row configuration; fewer would leave most of its tile
-  // empty, so they take the 128-row one.  The 128-row one also serves a
-  // batch whose 256-row work-groups would not reach one per CU (few requests
-  // and few kv heads, e.g. a head shard): twice the work-groups, so more CUs
-  // share the work.
-  int32_t rows = static_cast<int64_t>(max_extend_len) * grp >= 256 ? 256 : 128;
-  if (rows == 256) {
-    const int64_t items = static_cast<int64_t>(batch) * hkv * ((max_extend_len + 256 / grp - 1) / (256 / grp));
-    if (items < ra_device_cus()) rows = 128;
+  const ExtendPlan plan = extend_plan(batch, max_extend_len, hq / hkv, hkv, -1);
+  return extend_launch(q, k_new, v_new, total_tokens, k_pool, v_pool, pool_slots, req_to_token, rtt_rows, rtt_stride,
+                       req_pool_idx, prefix_lens, extend_lens, extend_start, batch, max_extend_len, hq, hkv, d,
+                       scale, out, plan, nullptr, stream);
+}
+
+extern "C" int32_t ra_extend_num_splits(int32_t batch, int32_t max_extend_len, int32_t hq, int32_t hkv,
+                                        int32_t num_splits) {
+  if (batch <= 0 || max_extend_len <= 0 || hq <= 0 || hkv <= 0 || hq % hkv != 0 || num_splits < 0) return 1;
+  return extend_plan(batch, max_extend_len, hq / hkv, hkv, num_splits).nsplit;
+}
+
+extern "C" size_t ra_extend_workspace_bytes(int64_t total_tokens, int32_t batch, int32_t max_extend_len, int32_t hq,
+                                            int32_t hkv, int32_t d, int32_t num_splits) {
+  if (total_tokens <= 0 || d <= 0) return 0;
+  const int32_t ns = ra_extend_num_splits(batch, max_extend_len, hq, hkv, num_splits);
+  if (ns <= 1) return 0;
+  return static_cast<size_t>(ns) * static_cast<size_t>(total_tokens) * hq * (d + 1) * sizeof(float);
+}
+
+extern "C" int ra_extend_attention_split(const void* q, const void* k_new, const void* v_new, int64_t total_tokens,
+                                         const void* k_pool, const void* v_pool, int64_t pool_slots,
+                                         const int32_t* req_to_token, int64_t rtt_rows, int64_t rtt_stride,
+                                         const int32_t* req_pool_idx, const int32_t* prefix_lens,
+                                         const int32_t* extend_lens, const int32_t* extend_start, int32_t batch,
+                                         int32_t max_extend_len, int32_t hq, int32_t hkv, int32_t d, float scale,
+                                         int32_t num_splits, void* workspace, size_t workspace_bytes, void* out,
+                                         hipStream_t stream) {
+  if (num_splits < 0) return ra_fail(RA_EINVAL, "ra_extend_attention_split: negative num_splits");
+  const int st = ra_extend_validate(q, k_new, v_new, total_tokens, k_pool, v_pool, pool_slots, req_to_token, rtt_rows,
+                                    rtt_stride, req_pool_idx, prefix_lens, extend_lens, extend_start, batch,
+                                    max_extend_len, hq, hkv, d, scale, out);
+  if (st != RA_OK || batch == 0 || max_extend_len == 0 || total_tokens == 0) return st;
+  const ExtendPlan plan = extend_plan(batch, max_extend_len, hq / hkv, hkv, num_splits);
+  if (plan.nsplit > 1) {
+    const size_t need = ra_extend_workspace_bytes(total_tokens, batch, max_extend_len, hq, hkv, d, num_splits);
+    if (workspace_bytes < need || !workspace)
+      return ra_fail(RA_EINVAL, "ra_extend_attention_split: workspace too small");
+    if (!ra_aligned16(workspace)) return ra_fail(RA_EINVAL, "ra_extend_attention_split: workspace alignment");
+  }
+  if (ra_debug_checks_enabled()) {
+    const int cst = ra_check_batch(req_to_token, rtt_rows, rtt_stride, pool_slots, req_pool_idx, batch, prefix_lens,
+                                   extend_lens, extend_start, total_tokens, max_extend_len, nullptr, 0, stream);
+    if (cst != RA_OK) return cst;
   }
   return extend_launch(q, k_new, v_new, total_tokens, k_pool, v_pool, pool_slots, req_to_token, rtt_rows, rtt_stride,
                        req_pool_idx, prefix_lens, extend_lens, extend_start, batch, max_extend_len, hq, hkv, d,
-                       scale, out, rows, stream);
+                       scale, out, plan, workspace, stream);
 }

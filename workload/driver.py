@@ -146,13 +146,23 @@ class ScenarioRun:
             pa.ra_store_kv(inp.new_slots, inp.k_new, inp.v_new, self.k_pool, self.v_pool)
             self.filled[inp.new_slots.cpu().numpy()] = True
 
-    def extend(self, inp: PhaseInputs, out=None):
+    def extend(self, inp: PhaseInputs, out=None, num_splits: int | None = None, workspace=None):
+        """ra_extend_attention, or ra_extend_attention_split when
+        ``num_splits`` is given (0: the library picks the key splits)."""
         if inp.n_ext == 0:
             return None
-        return pa.ra_extend_attention(
-            inp.q_ext, inp.k_new[: inp.total_ext], inp.v_new[: inp.total_ext], self.k_pool, self.v_pool,
-            inp.table, inp.rpi[: inp.n_ext], inp.prefix_lens, inp.extend_lens, inp.extend_start,
-            inp.max_extend_len, self.sc.scale, out=out)
+        args = (inp.q_ext, inp.k_new[: inp.total_ext], inp.v_new[: inp.total_ext], self.k_pool, self.v_pool,
+                inp.table, inp.rpi[: inp.n_ext], inp.prefix_lens, inp.extend_lens, inp.extend_start,
+                inp.max_extend_len, self.sc.scale)
+        if num_splits is None:
+            return pa.ra_extend_attention(*args, out=out)
+        return pa.ra_extend_attention_split(*args, num_splits=num_splits, workspace=workspace, out=out)
+
+    def extend_workspace_bytes(self, inp: PhaseInputs, num_splits: int = 0) -> int:
+        if inp.n_ext == 0:
+            return 0
+        return pa.ra_extend_workspace_bytes(inp.total_ext, inp.n_ext, inp.max_extend_len, self.sc.hq, self.sc.hkv,
+                                            self.sc.d, num_splits)
 
     def decode(self, inp: PhaseInputs, num_splits: int = 0, workspace=None, out=None):
         if inp.n_dec == 0:
@@ -161,10 +171,14 @@ class ScenarioRun:
             inp.q_dec, self.k_pool, self.v_pool, inp.table, inp.rpi[inp.n_ext:], inp.seq_lens, inp.max_seq_len,
             self.sc.scale, num_splits=num_splits, workspace=workspace, out=out)
 
-    def mixed(self, inp: PhaseInputs, num_splits: int = 0, workspace=None, out_ext=None, out_dec=None):
-        """Both halves of the batch in one ra_mixed_attention call."""
+    def mixed(self, inp: PhaseInputs, num_splits: int = 0, workspace=None, out_ext=None, out_dec=None,
+              ext_splits: int | None = None, ext_workspace=None):
+        """Both halves of the batch in one ra_mixed_attention call.  A batch
+        without decodes goes to the extend entry point, the split one when
+        ``ext_splits`` is given."""
         if inp.n_ext == 0 or inp.n_dec == 0:
-            return self.extend(inp, out=out_ext), self.decode(inp, num_splits, workspace, out_dec)
+            return (self.extend(inp, out=out_ext, num_splits=ext_splits, workspace=ext_workspace),
+                    self.decode(inp, num_splits, workspace, out_dec))
         return pa.ra_mixed_attention(
             inp.q_ext, inp.k_new[: inp.total_ext], inp.v_new[: inp.total_ext], inp.rpi[: inp.n_ext],
             inp.prefix_lens, inp.extend_lens, inp.extend_start, inp.max_extend_len, inp.q_dec,
