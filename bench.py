@@ -44,7 +44,7 @@ CSRC = os.path.join(ROOT, "paper_2312_07104_amd", "csrc")
 # sources whose code a kernel's launch runs (traffic figures are tied to them)
 KERNEL_SOURCES = {
     "extend": ["extend.hip", "lds_dma.h", "device_common.h"],
-    "decode": ["decode.hip", "lds_dma.h", "device_common.h"],
+    "decode": ["decode.hip", "decode_shared.hip", "lds_dma.h", "device_common.h"],
 }
 
 
@@ -221,6 +221,9 @@ def main():
                     help="oracle worker processes for the CPU baseline (one thread each)")
     ap.add_argument("--no-peaks", action="store_true", help="skip the machine-peak microbenchmarks")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--decode", choices=("shared", "per-request"), default="shared",
+                    help="decode half: shared-prefix plan (each shared run of the batch read once per block of "
+                         "requests) or one pass per request")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="after the timed loop, run one device copy of this size (HBM counter calibration)")
     args = ap.parse_args()
@@ -264,13 +267,38 @@ def main():
     ext_splits = 0 if inp.n_dec == 0 else None
     ext_ns = pa.ra_extend_num_splits(inp.n_ext, inp.max_extend_len, sc.hq, sc.hkv, 0) if ext_splits == 0 else 1
     log(f"[bench] extend key splits: {ext_ns}")
+    # Decode half from a shared-prefix plan, made on the host from the batch's
+    # slot rows before the timed region (its host time is reported).
+    use_shared = args.decode == "shared" and inp.n_dec > 0
+    plan = plan_dev = sh_ws = None
+    share = None
+    if use_shared:
+        plan, plan_dev = run.share_plan(inp)
+        sh_need = pa.ra_decode_shared_workspace_bytes(plan.n_parts, sc.hq, sc.d)
+        sh_ws = torch.empty(sh_need, dtype=torch.uint8, device="cuda") if sh_need else None
+        rows = plan.rows_per_kv_head * sc.hkv
+        # bytes the plan's items must move: K and V rows and slot indices of
+        # every item, queries, outputs, and each partial written and read once
+        plan_bytes = (rows * (2 * sc.d * 2 + 4) + inp.n_dec * 2 * sc.hq * sc.d * 2
+                      + 2 * plan.n_parts * sc.hq * (sc.d + 1) * 4)
+        share = {"members_per_item": plan.members_per_item, "chunk_len": plan.chunk_len, "items": plan.n_items,
+                 "partials": plan.n_parts, "rows_read": rows, "rows_per_request": work["sum_l"] * sc.hkv,
+                 "rows_read_fraction": rows / max(work["sum_l"] * sc.hkv, 1), "plan_bytes": plan_bytes,
+                 "host_plan_ms": run.share_plan_seconds * 1e3}
+        log(f"[bench] shared-prefix decode: {plan.n_items} items, {plan.n_parts} partials, "
+            f"{share['rows_read_fraction']:.3f} of the per-request rows, host plan {share['host_plan_ms']:.1f} ms")
     flush_buf = torch.empty(FLUSH_BYTES, dtype=torch.uint8, device="cuda")
 
     def step():
         """One pass of the hot path: store new K/V, then the mixed batch call."""
         if n_new:
             pa.ra_store_kv(inp.new_slots, inp.k_new, inp.v_new, run.k_pool, run.v_pool)
-        run.mixed(inp, workspace=ws_t, out_ext=out_e, out_dec=out_d, ext_splits=ext_splits, ext_workspace=ext_ws)
+        if use_shared:
+            run.mixed_shared(inp, plan, plan_dev, workspace=sh_ws, out_ext=out_e, out_dec=out_d,
+                             ext_splits=ext_splits, ext_workspace=ext_ws)
+        else:
+            run.mixed(inp, workspace=ws_t, out_ext=out_e, out_dec=out_d, ext_splits=ext_splits,
+                      ext_workspace=ext_ws)
 
     def step_sequential(ev):
         """The same work with each kernel timed alone (for the rooflines)."""
@@ -282,7 +310,10 @@ def main():
             run.extend(inp, out=out_e, num_splits=ext_splits, workspace=ext_ws)
         ev[2].record(stream)
         if inp.n_dec:
-            run.decode(inp, workspace=ws_t, out=out_d)
+            if use_shared:
+                run.decode_shared(inp, plan, plan_dev, workspace=sh_ws, out=out_d)
+            else:
+                run.decode(inp, workspace=ws_t, out=out_d)
         ev[3].record(stream)
 
     clock_steps = 0
@@ -321,7 +352,7 @@ def main():
                    "flops": work["ext_flops"], "gbs": work["ext_bytes"] / (t_ext * 1e-3) / 1e9,
                    "bytes": work["ext_bytes"], "unique_bytes": work["ext_unique_bytes"]} if inp.n_ext else None,
         "decode": {"ms": t_dec, "gbs": work["dec_bytes"] / (t_dec * 1e-3) / 1e9,
-                   "bytes": work["dec_bytes"]} if inp.n_dec else None,
+                   "bytes": work["dec_bytes"], "path": args.decode} if inp.n_dec else None,
     }
 
     def extend_roof():
@@ -337,9 +368,21 @@ def main():
                     "unit": "TFLOP/s"}
         return {"kernel": "extend", "bound": "hbm", "achieved": e["gbs"], "peak": HBM_PEAK_GBS, "unit": "GB/s"}
 
+    if share and kernels["decode"]:
+        kernels["decode"]["plan_bytes"] = share["plan_bytes"]
+        kernels["decode"]["plan_gbs"] = share["plan_bytes"] / (t_dec * 1e-3) / 1e9
+
     def decode_roof():
-        return {"kernel": "decode", "bound": "hbm", "achieved": kernels["decode"]["gbs"], "peak": HBM_PEAK_GBS,
-                "unit": "GB/s"}
+        """Decode is HBM-bound.  The shared-prefix path is priced on the bytes
+        its plan must move (each shared run once per block of requests); the
+        per-request byte rate, which counts every request's rows, is kept
+        beside it as logical_gbs."""
+        d = kernels["decode"]
+        r = {"kernel": "decode", "bound": "hbm", "achieved": d.get("plan_gbs", d["gbs"]), "peak": HBM_PEAK_GBS,
+             "unit": "GB/s"}
+        if "plan_gbs" in d:
+            r["logical_gbs"] = d["gbs"]
+        return r
 
     # roofline: the kernel that takes longer; roofline_other: the other one
     first, second = (extend_roof, decode_roof) if inp.n_ext and t_ext >= t_dec else (decode_roof, extend_roof)
@@ -396,6 +439,7 @@ def main():
                    "sum_extend_tokens": inp.total_ext, "sum_decode_context": work["sum_l"],
                    "history_requests": sc.history_len, "tree_calls": run.history_ops,
                    "hit_rate": inp.plan.hit_rate, "extend_key_splits": ext_ns if inp.n_ext else None,
+                   "decode_path": args.decode if inp.n_dec else None, "decode_share": share,
                    "parallelism": "none (1 GPU)"},
         "clock_warmup": {"seconds": args.clock_warmup, "steps": clock_steps},
         "ms_per_step_sequential_cold": ms_seq,

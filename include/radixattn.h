@@ -258,6 +258,59 @@ int ra_decode_attention_noalloc(const void* q, const void* k_pool, const void* v
                                 int32_t max_seq_len, int32_t hq, int32_t hkv, int32_t d, float scale,
                                 int32_t num_splits, void* out, hipStream_t stream);
 
+/* Shared-prefix decode.  With RadixAttention, requests that share a prefix
+ * hold the same pool slots for it (section 3), so a decode batch of requests
+ * on common branches of the radix tree reads the same K/V rows many times.
+ * ra_decode_share_plan (host, plain host pointers) finds those shared runs
+ * from the requests' slot rows: it sorts the requests by slot row, takes the
+ * tree of common-prefix intervals of neighbours, and turns every node with at
+ * least two requests and at least min_shared new positions into a shared
+ * segment; each request's rest is private.  Segments are cut into chunks of
+ * at most chunk_len positions and their requests into blocks of at most
+ * members_per_item (1 .. 16); every (chunk, block) is one work item,
+ * longest first.  chunk_len = 0 picks the longest of 4096, 2048, 1024, 512
+ * and 256 that still gives at least min_items items (e.g. two work-items'
+ * worth of waves per SIMD divided by Hkv; the shortest if none does).
+ *   req_to_token [rtt_rows, rtt_stride], req_pool_idx [B], seq_lens [B]:
+ *          host copies of the arrays ra_decode_attention takes (L clamped to
+ *          [0, rtt_stride]; requests with L = 0 get no item); RA_EINVAL for a
+ *          table row outside [0, rtt_rows)
+ *   plan:  int32 output of plan_capacity words; *plan_len receives the
+ *          length needed.  plan = NULL only queries the length; a shorter
+ *          buffer is RA_EINVAL.
+ * Plan layout: header of 16 words {n_items, n_member_entries, n_parts, B,
+ * members_per_item, rows per kv head, chunk length, 0...}, n_items items of 8 words
+ * {table row, first position, end position, first member entry, members,
+ * 0, 0, 0}, n_member_entries pairs {request, partial index or -1 for a
+ * request whose only item writes its output}, part_off [B + 1] (request b's
+ * partials are part_off[b] .. part_off[b+1]-1).
+ *
+ * ra_decode_attention_shared computes ra_decode_attention's output (query r
+ * over positions 0 .. L_r - 1) from such a plan, copied by the caller to
+ * device memory (`plan`, plan_len words, with the header's counts passed as
+ * n_items, n_member_entries, n_parts and members_per_item): one wave per
+ * (item, kv head) reads the item's K/V rows once for all its members' query
+ * heads (members_per_item x Hq / Hkv <= 64 MFMA columns), writes outputs of
+ * requests with one item directly and normalised partials with their
+ * log-sum-exp otherwise, and a second kernel merges each request's partials.
+ * workspace (16-byte aligned, caller-owned, contents undefined on return)
+ * must hold ra_decode_shared_workspace_bytes(n_parts, Hq, D) bytes.  Other
+ * arguments and layouts as ra_decode_attention; RA_EINVAL when plan_len does
+ * not match the counts.  Device-side bounds as ra_decode_attention: table
+ * rows, positions, requests and partial indices of the plan are clamped into
+ * their arrays. */
+int ra_decode_share_plan(const int32_t* req_to_token, int64_t rtt_rows, int64_t rtt_stride,
+                         const int32_t* req_pool_idx, const int32_t* seq_lens, int32_t batch,
+                         int32_t members_per_item, int32_t min_shared, int32_t chunk_len, int32_t min_items,
+                         int32_t* plan, int64_t plan_capacity, int64_t* plan_len);
+size_t ra_decode_shared_workspace_bytes(int32_t n_parts, int32_t hq, int32_t d);
+int ra_decode_attention_shared(const void* q, const void* k_pool, const void* v_pool, int64_t pool_slots,
+                               const int32_t* req_to_token, int64_t rtt_rows, int64_t rtt_stride, int32_t batch,
+                               int32_t hq, int32_t hkv, int32_t d, float scale, const int32_t* plan,
+                               int64_t plan_len, int32_t n_items, int32_t n_member_entries, int32_t n_parts,
+                               int32_t members_per_item, void* workspace, size_t workspace_bytes, void* out,
+                               hipStream_t stream);
+
 /* Batch validation (a debug aid).  The kernels keep every access inside
  * the arrays by clamping: a table row outside [0, rtt_rows) reads row 0, a
  * length above its bound is cut, a slot outside [0, pool_slots) reads the
@@ -280,9 +333,11 @@ int ra_check_batch(const int32_t* req_to_token, int64_t rtt_rows, int64_t rtt_st
                    int32_t max_extend_len, const int32_t* seq_lens, int32_t max_seq_len, hipStream_t stream);
 
 /* Debug switch for the whole library: while enabled (non-zero), every
- * ra_extend_attention, ra_decode_attention(_noalloc) and ra_mixed_attention
- * call runs ra_check_batch on its batch first (synchronising the stream) and
- * returns its error without launching anything.  Off by default. */
+ * ra_extend_attention(_split), ra_decode_attention(_noalloc) and
+ * ra_mixed_attention call runs ra_check_batch on its batch first
+ * (synchronising the stream) and returns its error without launching
+ * anything; ra_mixed_attention_shared checks its extend half (the shared
+ * decode's plan entries are clamped on the device).  Off by default. */
 int ra_set_debug_checks(int32_t enable);
 
 /* Mixed continuous batch (section 3: continuous batching merges new and
@@ -306,6 +361,21 @@ int ra_mixed_attention(const void* q_ext, const void* k_new, const void* v_new, 
                        void* out_dec, const void* k_pool, const void* v_pool, int64_t pool_slots,
                        const int32_t* req_to_token, int64_t rtt_rows, int64_t rtt_stride, int32_t hq,
                        int32_t hkv, int32_t d, float scale, hipStream_t stream);
+
+/* The same mixed batch with the decode half computed from a shared-prefix
+ * plan (ra_decode_share_plan, ra_decode_attention_shared): q_dec [n_dec, Hq,
+ * D], the plan's device words and header counts, its workspace and out_dec
+ * as ra_decode_attention_shared takes them.  Streams, ordering and the
+ * all-or-nothing argument checks as ra_mixed_attention. */
+int ra_mixed_attention_shared(const void* q_ext, const void* k_new, const void* v_new, int64_t total_tokens,
+                              const int32_t* req_pool_idx_ext, const int32_t* prefix_lens,
+                              const int32_t* extend_lens, const int32_t* extend_start, int32_t n_ext,
+                              int32_t max_extend_len, void* out_ext, const void* q_dec, int32_t n_dec,
+                              const int32_t* plan, int64_t plan_len, int32_t n_items, int32_t n_member_entries,
+                              int32_t n_parts, int32_t members_per_item, void* workspace, size_t workspace_bytes,
+                              void* out_dec, const void* k_pool, const void* v_pool, int64_t pool_slots,
+                              const int32_t* req_to_token, int64_t rtt_rows, int64_t rtt_stride, int32_t hq,
+                              int32_t hkv, int32_t d, float scale, hipStream_t stream);
 
 #ifdef __cplusplus
 }

@@ -68,6 +68,14 @@ _SIGS = {
     "ra_decode_noalloc_max_scratch_bytes": ([], ctypes.c_size_t),
     "ra_decode_attention_noalloc": ([_vp, _vp, _vp, _i64, _vp, _i64, _i64, _vp, _vp, _i32, _i32, _i32, _i32, _i32,
                                      ctypes.c_float, _i32, _vp, _vp], ctypes.c_int),
+    "ra_decode_share_plan": ([_vp, _i64, _i64, _vp, _vp, _i32, _i32, _i32, _i32, _i32, _vp, _i64, _i64p],
+                             ctypes.c_int),
+    "ra_decode_shared_workspace_bytes": ([_i32, _i32, _i32], ctypes.c_size_t),
+    "ra_decode_attention_shared": ([_vp, _vp, _vp, _i64, _vp, _i64, _i64, _i32, _i32, _i32, _i32, ctypes.c_float,
+                                    _vp, _i64, _i32, _i32, _i32, _i32, _vp, ctypes.c_size_t, _vp, _vp], ctypes.c_int),
+    "ra_mixed_attention_shared": ([_vp, _vp, _vp, _i64, _vp, _vp, _vp, _vp, _i32, _i32, _vp, _vp, _i32, _vp, _i64,
+                                   _i32, _i32, _i32, _i32, _vp, ctypes.c_size_t, _vp, _vp, _vp, _i64, _vp, _i64,
+                                   _i64, _i32, _i32, _i32, ctypes.c_float, _vp], ctypes.c_int),
     "ra_check_batch": ([_vp, _i64, _i64, _i64, _vp, _i32, _vp, _vp, _vp, _i64, _i32, _vp, _i32, _vp], ctypes.c_int),
     "ra_set_debug_checks": ([_i32], ctypes.c_int),
     "ra_mixed_attention": ([_vp, _vp, _vp, _i64, _vp, _vp, _vp, _vp, _i32, _i32, _vp,
@@ -388,6 +396,102 @@ def ra_decode_attention_noalloc(q, k_pool, v_pool, req_to_token, req_pool_idx, s
         _dev(seq_lens, torch.int32, "seq_lens"), b, int(max_seq_len), hq, hkv, d, float(scale), int(num_splits),
         _dev(out, torch.bfloat16, "out"), _stream(stream)))
     return out
+
+
+class SharePlan:
+    """A shared-prefix decode plan (ra_decode_share_plan) on the host, with
+    its header counts."""
+
+    def __init__(self, words: np.ndarray):
+        self.words = words
+        h = words[:16]
+        self.n_items, self.n_member_entries, self.n_parts = int(h[0]), int(h[1]), int(h[2])
+        self.batch, self.members_per_item, self.rows_per_kv_head = int(h[3]), int(h[4]), int(h[5])
+        self.chunk_len = int(h[6])
+        o = 16
+        self.items = words[o:o + 8 * self.n_items].reshape(-1, 8)
+        o += 8 * self.n_items
+        self.members = words[o:o + 2 * self.n_member_entries].reshape(-1, 2)
+        o += 2 * self.n_member_entries
+        self.part_off = words[o:o + self.batch + 1]
+
+
+def ra_decode_share_plan(req_to_token, req_pool_idx, seq_lens, members_per_item: int, min_shared: int = 256,
+                         chunk_len: int = 0, min_items: int = 0) -> SharePlan:
+    """Host plan of a shared-prefix decode batch from host copies (numpy) of
+    the slot table, the requests' table rows and their context lengths
+    (chunk_len 0: the longest chunk giving at least min_items items)."""
+    rtt = _np_i32(req_to_token)
+    rpi, sl = _np_i32(req_pool_idx), _np_i32(seq_lens)
+    if rtt.ndim != 2:
+        raise ValueError("req_to_token must be [rows, stride]")
+    n = ctypes.c_int64(0)
+    args = (rtt.ctypes.data, rtt.shape[0], rtt.shape[1], rpi.ctypes.data, sl.ctypes.data, rpi.shape[0],
+            int(members_per_item), int(min_shared), int(chunk_len), int(min_items))
+    _check(_lib.ra_decode_share_plan(*args, None, 0, ctypes.byref(n)))
+    words = np.zeros(n.value, dtype=np.int32)
+    _check(_lib.ra_decode_share_plan(*args, words.ctypes.data, words.shape[0], ctypes.byref(n)))
+    return SharePlan(words)
+
+
+def ra_decode_shared_workspace_bytes(n_parts: int, hq: int, d: int) -> int:
+    return int(_lib.ra_decode_shared_workspace_bytes(n_parts, hq, d))
+
+
+def ra_decode_attention_shared(q, k_pool, v_pool, req_to_token, plan: SharePlan, plan_dev, scale: float,
+                               workspace=None, out=None, stream=None):
+    """Decode attention over a shared-prefix plan; ``plan_dev`` is the plan's
+    words in device memory (int32)."""
+    import torch
+
+    b, hq, d = q.shape
+    hkv = k_pool.shape[1]
+    need = ra_decode_shared_workspace_bytes(plan.n_parts, hq, d)
+    if workspace is None and need:
+        workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
+    if out is None:
+        out = torch.empty_like(q)
+    ws_ptr = _dev(workspace, None, "workspace") if workspace is not None else None
+    ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    _check(_lib.ra_decode_attention_shared(
+        _dev(q, torch.bfloat16, "q"), _dev(k_pool, torch.bfloat16, "k_pool"), _dev(v_pool, torch.bfloat16, "v_pool"),
+        k_pool.shape[0], _dev(req_to_token, torch.int32, "req_to_token"), req_to_token.shape[0],
+        req_to_token.shape[1], b, hq, hkv, d, float(scale), _dev(plan_dev, torch.int32, "plan"),
+        plan_dev.numel(), plan.n_items, plan.n_member_entries, plan.n_parts, plan.members_per_item, ws_ptr,
+        ws_bytes, _dev(out, torch.bfloat16, "out"), _stream(stream)))
+    return out
+
+
+def ra_mixed_attention_shared(q_ext, k_new, v_new, req_pool_idx_ext, prefix_lens, extend_lens, extend_start,
+                              max_extend_len: int, q_dec, plan: SharePlan, plan_dev, k_pool, v_pool, req_to_token,
+                              scale: float, workspace=None, out_ext=None, out_dec=None, stream=None):
+    """ra_mixed_attention with the decode half from a shared-prefix plan."""
+    import torch
+
+    total, hq, d = q_ext.shape
+    hkv = k_pool.shape[1]
+    n_dec = q_dec.shape[0]
+    need = ra_decode_shared_workspace_bytes(plan.n_parts, hq, d)
+    if workspace is None and need:
+        workspace = torch.empty(need, dtype=torch.uint8, device=q_dec.device)
+    if out_ext is None:
+        out_ext = torch.empty_like(q_ext)
+    if out_dec is None:
+        out_dec = torch.empty_like(q_dec)
+    ws_ptr = _dev(workspace, None, "workspace") if workspace is not None else None
+    ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    _check(_lib.ra_mixed_attention_shared(
+        _dev(q_ext, torch.bfloat16, "q_ext"), _dev(k_new, torch.bfloat16, "k_new"),
+        _dev(v_new, torch.bfloat16, "v_new"), total, _dev(req_pool_idx_ext, torch.int32, "req_pool_idx_ext"),
+        _dev(prefix_lens, torch.int32, "prefix_lens"), _dev(extend_lens, torch.int32, "extend_lens"),
+        _dev(extend_start, torch.int32, "extend_start"), prefix_lens.shape[0], int(max_extend_len),
+        _dev(out_ext, torch.bfloat16, "out_ext"), _dev(q_dec, torch.bfloat16, "q_dec"), n_dec,
+        _dev(plan_dev, torch.int32, "plan"), plan_dev.numel(), plan.n_items, plan.n_member_entries, plan.n_parts,
+        plan.members_per_item, ws_ptr, ws_bytes, _dev(out_dec, torch.bfloat16, "out_dec"),
+        _dev(k_pool, torch.bfloat16, "k_pool"), _dev(v_pool, torch.bfloat16, "v_pool"), k_pool.shape[0],
+        _dev(req_to_token, torch.int32, "req_to_token"), req_to_token.shape[0], req_to_token.shape[1], hq, hkv, d,
+        float(scale), _stream(stream)))
+    return out_ext, out_dec
 
 
 def ra_check_batch(req_to_token, req_pool_idx, pool_slots: int, prefix_lens=None, extend_lens=None,

@@ -37,6 +37,28 @@ int companion_for(int device, Companion** out) {
   return RA_OK;
 }
 
+// Queues decode(companion stream) beside extend(stream): the companion waits
+// for the work already on the caller's stream, and the caller's stream waits
+// for the companion before anything queued after this call.
+template <class Decode, class Extend>
+int run_beside(hipStream_t stream, Decode&& decode, Extend&& extend) {
+  std::lock_guard<std::mutex> lock(g_mu);
+  int device = 0;
+  if (hipGetDevice(&device) != hipSuccess) return ra_fail(RA_EHIP, "ra_mixed_attention: hipGetDevice failed");
+  Companion* comp = nullptr;
+  int st = companion_for(device, &comp);
+  if (st != RA_OK) return st;
+  if (hipEventRecord(comp->fork, stream) != hipSuccess || hipStreamWaitEvent(comp->stream, comp->fork, 0) != hipSuccess)
+    return ra_fail(RA_EHIP, "ra_mixed_attention: cannot fork the companion stream");
+  st = decode(comp->stream);
+  if (st == RA_OK) st = extend(stream);
+  // Join even after a failed launch so the caller's stream never runs ahead
+  // of work already queued on the companion.
+  if (hipEventRecord(comp->join, comp->stream) != hipSuccess || hipStreamWaitEvent(stream, comp->join, 0) != hipSuccess)
+    return ra_fail(RA_EHIP, "ra_mixed_attention: cannot join the companion stream");
+  return st;
+}
+
 }  // namespace
 
 extern "C" int ra_mixed_attention(const void* q_ext, const void* k_new, const void* v_new, int64_t total_tokens,
@@ -77,24 +99,57 @@ extern "C" int ra_mixed_attention(const void* q_ext, const void* k_new, const vo
                               std::min<int64_t>(rtt_stride, INT32_MAX)), stream);
     if (st != RA_OK) return st;
   }
-  std::lock_guard<std::mutex> lock(g_mu);
-  int device = 0;
-  if (hipGetDevice(&device) != hipSuccess) return ra_fail(RA_EHIP, "ra_mixed_attention: hipGetDevice failed");
-  Companion* comp = nullptr;
-  st = companion_for(device, &comp);
-  if (st != RA_OK) return st;
-  if (hipEventRecord(comp->fork, stream) != hipSuccess || hipStreamWaitEvent(comp->stream, comp->fork, 0) != hipSuccess)
-    return ra_fail(RA_EHIP, "ra_mixed_attention: cannot fork the companion stream");
-  st = ra_decode_attention(q_dec, k_pool, v_pool, pool_slots, req_to_token, rtt_rows, rtt_stride, req_pool_idx_dec,
-                           seq_lens, n_dec, max_seq_len, hq, hkv, d, scale, num_splits, workspace, workspace_bytes,
-                           out_dec, comp->stream);
+  return run_beside(
+      stream,
+      [&](hipStream_t s) {
+        return ra_decode_attention(q_dec, k_pool, v_pool, pool_slots, req_to_token, rtt_rows, rtt_stride,
+                                   req_pool_idx_dec, seq_lens, n_dec, max_seq_len, hq, hkv, d, scale, num_splits,
+                                   workspace, workspace_bytes, out_dec, s);
+      },
+      [&](hipStream_t s) {
+        return ra_extend_attention(q_ext, k_new, v_new, total_tokens, k_pool, v_pool, pool_slots, req_to_token,
+                                   rtt_rows, rtt_stride, req_pool_idx_ext, prefix_lens, extend_lens, extend_start,
+                                   n_ext, max_extend_len, hq, hkv, d, scale, out_ext, s);
+      });
+}
+
+extern "C" int ra_mixed_attention_shared(const void* q_ext, const void* k_new, const void* v_new,
+                                         int64_t total_tokens, const int32_t* req_pool_idx_ext,
+                                         const int32_t* prefix_lens, const int32_t* extend_lens,
+                                         const int32_t* extend_start, int32_t n_ext, int32_t max_extend_len,
+                                         void* out_ext, const void* q_dec, int32_t n_dec, const int32_t* plan,
+                                         int64_t plan_len, int32_t n_items, int32_t n_member_entries,
+                                         int32_t n_parts, int32_t members_per_item, void* workspace,
+                                         size_t workspace_bytes, void* out_dec, const void* k_pool,
+                                         const void* v_pool, int64_t pool_slots, const int32_t* req_to_token,
+                                         int64_t rtt_rows, int64_t rtt_stride, int32_t hq, int32_t hkv, int32_t d,
+                                         float scale, hipStream_t stream) {
+  if (n_ext < 0 || n_dec < 0) return ra_fail(RA_EINVAL, "ra_mixed_attention_shared: negative batch");
+  auto decode = [&](hipStream_t s) {
+    return ra_decode_attention_shared(q_dec, k_pool, v_pool, pool_slots, req_to_token, rtt_rows, rtt_stride, n_dec,
+                                      hq, hkv, d, scale, plan, plan_len, n_items, n_member_entries, n_parts,
+                                      members_per_item, workspace, workspace_bytes, out_dec, s);
+  };
+  auto extend = [&](hipStream_t s) {
+    return ra_extend_attention(q_ext, k_new, v_new, total_tokens, k_pool, v_pool, pool_slots, req_to_token, rtt_rows,
+                               rtt_stride, req_pool_idx_ext, prefix_lens, extend_lens, extend_start, n_ext,
+                               max_extend_len, hq, hkv, d, scale, out_ext, s);
+  };
+  if (n_dec == 0 || n_items == 0) return extend(stream);
+  if (n_ext == 0 || max_extend_len == 0 || total_tokens == 0) return decode(stream);
+  // Check both halves before queuing either, so a failing call changes nothing.
+  int st = ra_extend_validate(q_ext, k_new, v_new, total_tokens, k_pool, v_pool, pool_slots, req_to_token, rtt_rows,
+                              rtt_stride, req_pool_idx_ext, prefix_lens, extend_lens, extend_start, n_ext,
+                              max_extend_len, hq, hkv, d, scale, out_ext);
   if (st == RA_OK)
-    st = ra_extend_attention(q_ext, k_new, v_new, total_tokens, k_pool, v_pool, pool_slots, req_to_token, rtt_rows,
-                             rtt_stride, req_pool_idx_ext, prefix_lens, extend_lens, extend_start, n_ext,
-                             max_extend_len, hq, hkv, d, scale, out_ext, stream);
-  // Join even after a failed launch so the caller's stream never runs ahead
-  // of work already queued on the companion.
-  if (hipEventRecord(comp->join, comp->stream) != hipSuccess || hipStreamWaitEvent(stream, comp->join, 0) != hipSuccess)
-    return ra_fail(RA_EHIP, "ra_mixed_attention: cannot join the companion stream");
-  return st;
+    st = ra_decode_shared_validate(q_dec, k_pool, v_pool, pool_slots, req_to_token, rtt_rows, rtt_stride, n_dec, hq,
+                                   hkv, d, scale, plan, plan_len, n_items, n_member_entries, n_parts,
+                                   members_per_item, workspace, workspace_bytes, out_dec);
+  if (st != RA_OK) return st;
+  if (ra_debug_checks_enabled()) {
+    st = ra_check_batch(req_to_token, rtt_rows, rtt_stride, pool_slots, req_pool_idx_ext, n_ext, prefix_lens,
+                        extend_lens, extend_start, total_tokens, max_extend_len, nullptr, 0, stream);
+    if (st != RA_OK) return st;
+  }
+  return run_beside(stream, decode, extend);
 }

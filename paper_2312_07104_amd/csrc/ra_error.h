@@ -50,6 +50,12 @@ int ra_decode_validate(const void* q, const void* k_pool, const void* v_pool, in
                        float scale, int32_t num_splits, const void* workspace, size_t workspace_bytes,
                        const void* out);
 
+int ra_decode_shared_validate(const void* q, const void* k_pool, const void* v_pool, int64_t pool_slots,
+                              const int32_t* req_to_token, int64_t rtt_rows, int64_t rtt_stride, int32_t batch,
+                              int32_t hq, int32_t hkv, int32_t d, float scale, const int32_t* plan, int64_t plan_len,
+                              int32_t n_items, int32_t n_member_entries, int32_t n_parts, int32_t members_per_item,
+                              const void* workspace, size_t workspace_bytes, const void* out);
+
 // True while ra_set_debug_checks(1) is in force: the attention entry points
 // then run ra_check_batch on their batch before launching.
 bool ra_debug_checks_enabled();

@@ -171,6 +171,47 @@ class ScenarioRun:
             inp.q_dec, self.k_pool, self.v_pool, inp.table, inp.rpi[inp.n_ext:], inp.seq_lens, inp.max_seq_len,
             self.sc.scale, num_splits=num_splits, workspace=workspace, out=out)
 
+    def share_plan(self, inp: PhaseInputs, members_per_item: int | None = None, min_shared: int = 256,
+                   chunk_len: int = 0, min_items: int | None = None):
+        """Host plan of the decode half for ra_decode_attention_shared (from
+        host copies of the table, the decode requests' rows and lengths) and
+        its words in device memory.  Defaults: members_per_item fills two
+        16-column MFMA blocks with query heads (32 / G requests, 1 .. 16);
+        chunk_len 0 with min_items = three waves per SIMD over the kv heads."""
+        grp = self.sc.hq // self.sc.hkv
+        if members_per_item is None:
+            members_per_item = max(1, min(16, 32 // grp))
+        if min_items is None:
+            cus = torch.cuda.get_device_properties(0).multi_processor_count if torch.cuda.is_available() else 256
+            min_items = -(-3 * 4 * cus // self.sc.hkv)
+        t0 = time.perf_counter()
+        plan = pa.ra_decode_share_plan(inp.table.cpu().numpy(), inp.rpi[inp.n_ext:].cpu().numpy(),
+                                       inp.seq_lens.cpu().numpy(), members_per_item, min_shared, chunk_len,
+                                       min_items)
+        self.share_plan_seconds = time.perf_counter() - t0
+        return plan, torch.from_numpy(plan.words).to(self.device)
+
+    def decode_shared(self, inp: PhaseInputs, plan, plan_dev, workspace=None, out=None):
+        if inp.n_dec == 0:
+            return None
+        return pa.ra_decode_attention_shared(inp.q_dec, self.k_pool, self.v_pool, inp.table, plan, plan_dev,
+                                             self.sc.scale, workspace=workspace, out=out)
+
+    def mixed_shared(self, inp: PhaseInputs, plan, plan_dev, workspace=None, out_ext=None, out_dec=None,
+                     ext_splits: int | None = None, ext_workspace=None):
+        """Both halves in one ra_mixed_attention_shared call (the decode half
+        from a shared-prefix plan).  A batch without extends or decodes goes
+        to the one entry point it needs."""
+        if inp.n_dec == 0:
+            return self.extend(inp, out=out_ext, num_splits=ext_splits, workspace=ext_workspace), None
+        if inp.n_ext == 0:
+            return None, self.decode_shared(inp, plan, plan_dev, workspace=workspace, out=out_dec)
+        return pa.ra_mixed_attention_shared(
+            inp.q_ext, inp.k_new[: inp.total_ext], inp.v_new[: inp.total_ext], inp.rpi[: inp.n_ext],
+            inp.prefix_lens, inp.extend_lens, inp.extend_start, inp.max_extend_len, inp.q_dec, plan, plan_dev,
+            self.k_pool, self.v_pool, inp.table, self.sc.scale, workspace=workspace, out_ext=out_ext,
+            out_dec=out_dec)
+
     def mixed(self, inp: PhaseInputs, num_splits: int = 0, workspace=None, out_ext=None, out_dec=None,
               ext_splits: int | None = None, ext_workspace=None):
         """Both halves of the batch in one ra_mixed_attention call.  A batch
