@@ -56,9 +56,11 @@ def sources_sha256(kernel):
     return h.hexdigest()
 
 
-def measured_traffic(kernel, workload):
-    """HBM bytes per launch from the committed counter summary, or None when
-    it is missing or was taken on different kernel sources."""
+def measured_traffic(kernel, workload, decode_path=None):
+    """HBM bytes per step of a kernel (all its launches in the step: the
+    partial pass and its combine) from the committed counter summary, or None
+    when it is missing, was taken on different kernel sources or, for decode,
+    on the other decode path."""
     path = os.path.join(ROOT, "profiles", "traffic.json")
     try:
         with open(path) as fh:
@@ -66,6 +68,8 @@ def measured_traffic(kernel, workload):
     except (OSError, ValueError):
         return None
     if not rec or rec.get("sources_sha256") != sources_sha256(kernel):
+        return None
+    if kernel == "decode" and rec.get("decode_path") != decode_path:
         return None
     return rec.get("hbm_bytes_per_launch")
 
@@ -395,7 +399,7 @@ def main():
     for r in (roof, other):
         if r:
             r["frac"] = r["achieved"] / r["peak"]
-            r["traffic"] = measured_traffic(r["kernel"], sc.name)
+            r["traffic"] = measured_traffic(r["kernel"], sc.name, args.decode)
             # HBM bytes the counters saw per launch over the kernel's duration
             if r["traffic"]:
                 r["hbm_gbs"] = r["traffic"] / (kernels[r["kernel"]]["ms"] * 1e-3) / 1e9

@@ -177,13 +177,13 @@ class ScenarioRun:
         host copies of the table, the decode requests' rows and lengths) and
         its words in device memory.  Defaults: members_per_item fills two
         16-column MFMA blocks with query heads (32 / G requests, 1 .. 16);
-        chunk_len 0 with min_items = three waves per SIMD over the kv heads."""
+        chunk_len 0 with min_items = one wave per SIMD over the kv heads."""
         grp = self.sc.hq // self.sc.hkv
         if members_per_item is None:
             members_per_item = max(1, min(16, 32 // grp))
         if min_items is None:
             cus = torch.cuda.get_device_properties(0).multi_processor_count if torch.cuda.is_available() else 256
-            min_items = -(-3 * 4 * cus // self.sc.hkv)
+            min_items = -(-4 * cus // self.sc.hkv)
         t0 = time.perf_counter()
         plan = pa.ra_decode_share_plan(inp.table.cpu().numpy(), inp.rpi[inp.n_ext:].cpu().numpy(),
                                        inp.seq_lens.cpu().numpy(), members_per_item, min_shared, chunk_len,
