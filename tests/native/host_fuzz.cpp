@@ -4,7 +4,9 @@
 // small vocabulary (so sequences share prefixes): match, lock, allocate
 // (evicting on shortage, as Algorithm 1 does), insert, unlock, drain the
 // eviction log into the router, and check that every slot is either free or
-// held by the tree.  Exits non-zero on the first failed check.
+// held by the tree; then plan random batches of slot rows for the
+// shared-prefix decode and check the plans' coverage.  Exits non-zero on the
+// first failed check.
 #include <algorithm>
 #include <cstdint>
 #include <cstdio>
@@ -101,10 +103,93 @@ static int run_seed(int seed) {
   return 0;
 }
 
+// The shared-prefix decode planner on a batch of slot rows drawn from a
+// random tree of slot runs (shared runs, identical rows, rows that are
+// prefixes of others, empty contexts, permuted table rows): every request's
+// positions covered exactly once, members' rows equal over their items,
+// partial indices consecutive per request; a short buffer is rejected.
+static int plan_seed(int seed) {
+  std::mt19937_64 rng(0x5eed0000u + static_cast<uint64_t>(seed));
+  const int32_t B = 1 + static_cast<int32_t>(rng() % 40);
+  std::vector<std::vector<int32_t>> runs;  // node k's slot run; parent of k is k / 3 (k > 0)
+  int32_t next = 100;
+  for (int k = 0; k < 40; ++k) {
+    std::vector<int32_t> r(1 + rng() % 30);
+    for (auto& x : r) x = next++;
+    runs.push_back(r);
+  }
+  std::vector<std::vector<int32_t>> rows(static_cast<size_t>(B));
+  for (int32_t b = 0; b < B; ++b) {
+    int node = static_cast<int>(rng() % runs.size());
+    std::vector<int> path;
+    for (; node > 0; node /= 3) path.push_back(node);
+    for (auto it = path.rbegin(); it != path.rend(); ++it) rows[b].insert(rows[b].end(), runs[*it].begin(), runs[*it].end());
+    if (b > 0 && rng() % 8 == 0) rows[b] = rows[rng() % b];                      // identical row
+    if (rng() % 5 == 0) rows[b].resize(rng() % (rows[b].size() + 1));          // cut (maybe empty)
+    for (int k = static_cast<int>(rng() % 6); k > 0; --k) rows[b].push_back(next++);  // private tail
+  }
+  size_t stride = 1;
+  for (auto& r : rows) stride = std::max(stride, r.size() + 2);
+  const int64_t R = B + 3;
+  std::vector<int32_t> rtt(static_cast<size_t>(R) * stride, -9), rpi(B), lens(B);
+  for (int32_t b = 0; b < B; ++b) {
+    rpi[b] = (b * 7 + 2) % static_cast<int32_t>(R);
+    while (std::count(rpi.begin(), rpi.begin() + b, rpi[b])) rpi[b] = (rpi[b] + 1) % static_cast<int32_t>(R);
+    std::copy(rows[b].begin(), rows[b].end(), rtt.begin() + static_cast<int64_t>(rpi[b]) * stride);
+    lens[b] = static_cast<int32_t>(rows[b].size());
+  }
+  const int32_t mpb = 1 + static_cast<int32_t>(rng() % 16), min_shared = 1 + static_cast<int32_t>(rng() % 20);
+  const int32_t chunk = static_cast<int32_t>(rng() % 3 == 0 ? 0 : 1 + rng() % 40);
+  int64_t need = 0;
+  CHECK(ra_decode_share_plan(rtt.data(), R, static_cast<int64_t>(stride), rpi.data(), lens.data(), B, mpb, min_shared,
+                             chunk, 8, nullptr, 0, &need) == RA_OK);
+  std::vector<int32_t> plan(static_cast<size_t>(need));
+  if (need > 1)
+    CHECK(ra_decode_share_plan(rtt.data(), R, static_cast<int64_t>(stride), rpi.data(), lens.data(), B, mpb,
+                               min_shared, chunk, 8, plan.data(), need - 1, &need) == RA_EINVAL);
+  CHECK(ra_decode_share_plan(rtt.data(), R, static_cast<int64_t>(stride), rpi.data(), lens.data(), B, mpb, min_shared,
+                             chunk, 8, plan.data(), need, &need) == RA_OK);
+  const int32_t n_items = plan[0], n_mem = plan[1], n_parts = plan[2];
+  CHECK(plan[3] == B && plan[4] == mpb && need == 16 + 8 * int64_t{n_items} + 2 * int64_t{n_mem} + B + 1);
+  const int32_t* items = plan.data() + 16;
+  const int32_t* mem = items + 8 * static_cast<int64_t>(n_items);
+  const int32_t* part_off = mem + 2 * static_cast<int64_t>(n_mem);
+  std::vector<std::vector<int>> cover(static_cast<size_t>(B));
+  std::vector<std::vector<int32_t>> parts(static_cast<size_t>(B));
+  for (int32_t b = 0; b < B; ++b) cover[b].assign(static_cast<size_t>(lens[b]), 0);
+  for (int32_t i = 0; i < n_items; ++i) {
+    const int32_t* it = items + 8 * i;
+    CHECK(it[0] >= 0 && it[0] < R && 0 <= it[1] && it[1] < it[2] && it[4] >= 1 && it[4] <= mpb);
+    CHECK(it[3] >= 0 && it[3] + it[4] <= n_mem);
+    for (int32_t m = 0; m < it[4]; ++m) {
+      const int32_t b = mem[2 * (it[3] + m)];
+      CHECK(b >= 0 && b < B && it[2] <= lens[b]);
+      for (int32_t t = it[1]; t < it[2]; ++t) {
+        CHECK(rtt[static_cast<size_t>(rpi[b]) * stride + t] == rtt[static_cast<size_t>(it[0]) * stride + t]);
+        ++cover[b][t];
+      }
+      parts[b].push_back(mem[2 * (it[3] + m) + 1]);
+    }
+  }
+  CHECK(part_off[0] == 0 && part_off[B] == n_parts);
+  for (int32_t b = 0; b < B; ++b) {
+    for (int c : cover[b]) CHECK(c == 1);
+    const int32_t lo = part_off[b], hi = part_off[b + 1];
+    if (parts[b].size() == 1) {
+      CHECK(parts[b][0] == -1 && hi == lo);
+    } else {
+      std::sort(parts[b].begin(), parts[b].end());
+      CHECK(static_cast<int32_t>(parts[b].size()) == hi - lo);
+      for (size_t k = 0; k < parts[b].size(); ++k) CHECK(parts[b][k] == lo + static_cast<int32_t>(k));
+    }
+  }
+  return 0;
+}
+
 int main(int argc, char** argv) {
   const int seeds = argc > 1 ? std::atoi(argv[1]) : 20;
   for (int s = 0; s < seeds; ++s)
-    if (run_seed(s) != 0) {
+    if (run_seed(s) != 0 || plan_seed(s) != 0) {
       std::fprintf(stderr, "seed %d failed\n", s);
       return 1;
     }

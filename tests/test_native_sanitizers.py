@@ -1,7 +1,9 @@
-"""The host C++ (radix cache, eviction log, router) under AddressSanitizer and
-UndefinedBehaviorSanitizer: tests/native/host_fuzz.cpp drives seeded random
-request streams through the C ABI and checks slot accounting after every
-request.  Host code only, built with g++ (no GPU code is involved)."""
+"""The host C++ (radix cache, eviction log, router, shared-prefix decode
+planner) under AddressSanitizer and UndefinedBehaviorSanitizer:
+tests/native/host_fuzz.cpp drives seeded random request streams through the
+C ABI and checks slot accounting after every request, and plans random
+batches of slot rows and checks their coverage.  Host code only, built with
+g++ (no GPU code is involved)."""
 import os
 import shutil
 import subprocess
@@ -21,7 +23,7 @@ def test_host_code_clean_under_asan_and_ubsan(tmp_path):
            "-fno-omit-frame-pointer", "-D__HIP_PLATFORM_AMD__", f"-I{ROOT}/include", f"-I{CSRC}",
            "-I/opt/rocm/include", os.path.join(ROOT, "tests", "native", "host_fuzz.cpp"),
            os.path.join(CSRC, "radix_cache.cpp"), os.path.join(CSRC, "router.cpp"),
-           os.path.join(CSRC, "ra_error.cpp"), "-o", exe]
+           os.path.join(CSRC, "ra_error.cpp"), os.path.join(CSRC, "share_plan.cpp"), "-o", exe]
     b = subprocess.run(cmd, capture_output=True, text=True, timeout=600)
     if b.returncode != 0 and "hip" in b.stderr and "No such file" in b.stderr:
         pytest.skip("HIP headers not available for a host-only build")
