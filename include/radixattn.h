@@ -94,7 +94,9 @@ int ra_free_slots(ra_cache* c, const int32_t* slots, int64_t n);
  * from the cached one at the same position is returned to the pool.  Splits
  * an edge where the sequence diverges inside it.  *out_cached = positions
  * that were already cached, *out_node = node ending at position n (either may
- * be NULL).  The new leaf is unreferenced (evictable). */
+ * be NULL).  The new leaf is unreferenced (evictable).  EINVAL (no effect)
+ * for n >= 2^31, a new slot that is out of range or free, or differing
+ * caller slots that are out of range, free or repeated. */
 int ra_insert(ra_cache* c, const int32_t* tokens, const int32_t* slots, int64_t n,
               int64_t* out_cached, int64_t* out_node);
 

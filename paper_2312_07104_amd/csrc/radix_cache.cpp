@@ -13,10 +13,15 @@
 //  * the pool is a FIFO queue with a caller-given initial order.
 //
 // Data layout for large trees (hundreds of thousands of operations over
-// millions of tokens): nodes live in a vector indexed by id; the child edge
-// index is one hash map keyed by (parent id, first token); the evictable
-// leaves are an ordered set keyed by (stamp, id), kept current on every
-// change, so eviction never scans the tree.
+// millions of tokens, where requests that end inside shared text cut the
+// shared edges into runs of a few tokens, so a walk crosses hundreds of
+// edges): nodes live in a vector indexed by id, one cache line each, with
+// the edge's tokens and slots in one buffer; the child edge index is one
+// open-addressing table keyed by (parent id, first token), whose entry for
+// the next edge is fetched while the current edge is compared; the free map
+// is one bit per slot; the evictable leaves are an ordered set keyed by
+// (stamp, id), kept current on every change, so eviction never scans the
+// tree.
 #include <algorithm>
 #include <cstdint>
 #include <cstring>
@@ -24,7 +29,6 @@
 #include <memory>
 #include <set>
 #include <string>
-#include <unordered_map>
 #include <vector>
 
 #include "radixattn.h"
@@ -32,21 +36,108 @@
 
 namespace {
 
-struct Node {
+struct alignas(64) Node {
   int64_t parent = -1;
-  std::vector<int32_t> key;
-  std::vector<int32_t> slots;
-  int64_t ref = 0;
   uint64_t stamp = 0;
-  int64_t n_children = 0;
-  bool alive = false;
-  bool in_lru = false;   // present in the evictable-leaf set
   uint64_t lru_stamp = 0;  // stamp it was filed under
+  int64_t ref = 0;
+  int32_t len = 0;         // tokens on the edge into this node
+  int32_t n_children = 0;
+  bool alive = false;
+  bool in_lru = false;     // present in the evictable-leaf set
+  std::unique_ptr<int32_t[]> kv;  // the edge's tokens, then their slots
+  const int32_t* key() const { return kv.get(); }
+  const int32_t* slots() const { return kv.get() + len; }
+  void assign(const int32_t* k, const int32_t* s, int64_t n) {
+    std::unique_ptr<int32_t[]> b(new int32_t[2 * n]);
+    std::memcpy(b.get(), k, n * sizeof(int32_t));
+    std::memcpy(b.get() + n, s, n * sizeof(int32_t));
+    kv = std::move(b);
+    len = static_cast<int32_t>(n);
+  }
 };
 
 inline uint64_t edge_key(int64_t parent, int32_t tok) {
   return (static_cast<uint64_t>(parent) << 32) ^ static_cast<uint32_t>(tok);
 }
+
+
+// Open-addressing map from edge key to child id: linear probing over a
+// power-of-two table at most 3/4 full, deletion by backward shift (no
+// tombstones).  The slot hash is the 64-bit finalizer of MurmurHash3.
+class EdgeMap {
+ public:
+  EdgeMap() { rehash(1024); }
+  int64_t find(uint64_t k) const {
+    size_t i = slot(k);
+    for (;;) {
+      const Entry& e = tab_[i];
+      if (e.key == k) return e.val;
+      if (e.key == kEmpty) return -1;
+      i = (i + 1) & mask_;
+    }
+  }
+  void set(uint64_t k, int64_t v) {
+    if ((size_ + 1) * 4 > tab_.size() * 3) rehash(tab_.size() * 2);
+    size_t i = slot(k);
+    for (;;) {
+      Entry& e = tab_[i];
+      if (e.key == k) { e.val = v; return; }
+      if (e.key == kEmpty) { e.key = k; e.val = v; ++size_; return; }
+      i = (i + 1) & mask_;
+    }
+  }
+  void erase(uint64_t k) {
+    size_t i = slot(k);
+    for (;;) {
+      if (tab_[i].key == kEmpty) return;
+      if (tab_[i].key == k) break;
+      i = (i + 1) & mask_;
+    }
+    // shift later members of the probe run back into the hole
+    size_t hole = i;
+    for (size_t j = (i + 1) & mask_;; j = (j + 1) & mask_) {
+      if (tab_[j].key == kEmpty) break;
+      size_t home = slot(tab_[j].key);
+      // j's entry may fill the hole if its home is not in (hole, j]
+      bool movable = hole <= j ? (home <= hole || home > j) : (home <= hole && home > j);
+      if (movable) { tab_[hole] = tab_[j]; hole = j; }
+    }
+    tab_[hole].key = kEmpty;
+    --size_;
+  }
+  // starts fetching the probe run of k (a lookup that follows soon)
+  void prefetch(uint64_t k) const { __builtin_prefetch(&tab_[slot(k)]); }
+ private:
+  static constexpr uint64_t kEmpty = ~0ull;
+  struct Entry { uint64_t key; int64_t val; };
+  size_t slot(uint64_t k) const {
+    k ^= k >> 33; k *= 0xff51afd7ed558ccdull; k ^= k >> 33;
+    return static_cast<size_t>(k) & mask_;
+  }
+  void rehash(size_t cap) {
+    std::vector<Entry> old;
+    old.swap(tab_);
+    tab_.assign(cap, Entry{kEmpty, 0});
+    mask_ = cap - 1;
+    size_ = 0;
+    for (const Entry& e : old)
+      if (e.key != kEmpty) set(e.key, e.val);
+  }
+  std::vector<Entry> tab_;
+  size_t mask_ = 0, size_ = 0;
+};
+
+// One bit per pool slot: set while the slot is in the free queue.
+class SlotBits {
+ public:
+  void reset(size_t n) { w_.assign((n + 63) / 64, 0); }
+  bool get(int32_t s) const { return (w_[static_cast<uint32_t>(s) >> 6] >> (s & 63)) & 1; }
+  void set(int32_t s) { w_[static_cast<uint32_t>(s) >> 6] |= 1ull << (s & 63); }
+  void clr(int32_t s) { w_[static_cast<uint32_t>(s) >> 6] &= ~(1ull << (s & 63)); }
+ private:
+  std::vector<uint64_t> w_;
+};
 
 }  // namespace
 
@@ -55,10 +146,10 @@ struct ra_cache {
   // FIFO free queue as a ring buffer of capacity pool_slots
   std::vector<int32_t> ring;
   int64_t head = 0, count = 0;
-  std::vector<uint8_t> is_free;
+  SlotBits is_free;
 
   std::vector<Node> nodes;
-  std::unordered_map<uint64_t, int64_t> children;  // (parent, first token) -> child
+  EdgeMap children;  // (parent, first token) -> child
   std::set<std::pair<uint64_t, int64_t>> lru;      // evictable leaves
   uint64_t clock = 0;
   int64_t live = 1;
@@ -100,27 +191,26 @@ struct ra_cache {
     if (at >= pool_slots) at -= pool_slots;
     ring[at] = s;
     ++count;
-    is_free[s] = 1;
+    is_free.set(s);
   }
   int32_t pop_free() {
     int32_t s = ring[head];
     if (++head == pool_slots) head = 0;
     --count;
-    is_free[s] = 0;
+    is_free.clr(s);
     return s;
   }
 
   // ---- tree ----
   // Appends a node.  key and slots are taken by value: callers may pass
   // views into another node, which the vector growth below would invalidate.
-  int64_t new_node(int64_t parent, std::vector<int32_t> key, std::vector<int32_t> slots,
+  int64_t new_node(int64_t parent, const int32_t* key, const int32_t* slots, int64_t len,
                    int64_t ref, uint64_t stamp) {
     int64_t id = static_cast<int64_t>(nodes.size());
     nodes.emplace_back();
     Node& n = nodes.back();
     n.parent = parent;
-    n.key = std::move(key);
-    n.slots = std::move(slots);
+    n.assign(key, slots, len);
     n.ref = ref;
     n.stamp = stamp;
     n.alive = true;
@@ -131,18 +221,15 @@ struct ra_cache {
   // Splits node x after c tokens; returns the new upper node.
   int64_t split(int64_t x, int64_t c) {
     int64_t par = nodes[x].parent;
-    int32_t first = nodes[x].key[0];
-    int64_t y = new_node(par, std::vector<int32_t>(nodes[x].key.begin(), nodes[x].key.begin() + c),
-                         std::vector<int32_t>(nodes[x].slots.begin(), nodes[x].slots.begin() + c),
-                         nodes[x].ref, nodes[x].stamp);
+    int32_t first = nodes[x].key()[0];
+    int64_t y = new_node(par, nodes[x].key(), nodes[x].slots(), c, nodes[x].ref, nodes[x].stamp);
     Node& X = nodes[x];
     Node& Y = nodes[y];
-    X.key.erase(X.key.begin(), X.key.begin() + c);
-    X.slots.erase(X.slots.begin(), X.slots.begin() + c);
+    X.assign(X.key() + c, X.slots() + c, X.len - c);
     X.parent = y;
     Y.n_children = 1;
-    children[edge_key(par, first)] = y;
-    children[edge_key(y, X.key[0])] = x;
+    children.set(edge_key(par, first), y);
+    children.set(edge_key(y, X.key()[0]), x);
     refresh(x);
     refresh(y);
     return y;
@@ -154,14 +241,17 @@ struct ra_cache {
     ++clock;
     int64_t node = 0, pos = 0;
     while (pos < n) {
-      auto it = children.find(edge_key(node, tok[pos]));
-      if (it == children.end()) break;
-      int64_t ch = it->second;
-      const std::vector<int32_t>& key = nodes[ch].key;
-      int64_t lim = std::min<int64_t>(static_cast<int64_t>(key.size()), n - pos);
+      int64_t ch = children.find(edge_key(node, tok[pos]));
+      if (ch < 0) break;
+      const Node& cn = nodes[ch];
+      const int32_t* key = cn.key();
+      const int64_t klen = cn.len;
+      if (pos + klen < n) children.prefetch(edge_key(ch, tok[pos + klen]));
+      __builtin_prefetch(key);
+      int64_t lim = std::min<int64_t>(klen, n - pos);
       int64_t c = 0;
       while (c < lim && key[c] == tok[pos + c]) ++c;
-      if (c < static_cast<int64_t>(key.size())) ch = split(ch, c);
+      if (c < klen) ch = split(ch, c);
       nodes[ch].stamp = clock;
       refresh(ch);
       visit(ch, pos);
@@ -183,10 +273,10 @@ int ra_cache_create(int64_t pool_slots, const int32_t* order, ra_cache** out) {
     std::unique_ptr<ra_cache> c(new ra_cache());
     c->pool_slots = pool_slots;
     c->ring.resize(static_cast<size_t>(pool_slots));
-    c->is_free.assign(static_cast<size_t>(pool_slots), 0);
+    c->is_free.reset(static_cast<size_t>(pool_slots));
     for (int64_t i = 0; i < pool_slots; ++i) {
       int32_t s = order ? order[i] : static_cast<int32_t>(i);
-      if (s < 0 || s >= pool_slots || c->is_free[s])
+      if (s < 0 || s >= pool_slots || c->is_free.get(s))
         return ra_fail(RA_EINVAL, "ra_cache_create: initial order is not a permutation");
       c->push_free(s);
     }
@@ -206,8 +296,8 @@ int ra_match_prefix(ra_cache* c, const int32_t* tokens, int64_t n, int32_t* out_
     int64_t pos = 0;
     int64_t node = c->walk(tokens, n, &pos, [&](int64_t ch, int64_t p) {
       if (out_slots) {
-        const auto& s = c->nodes[ch].slots;
-        std::memcpy(out_slots + p, s.data(), s.size() * sizeof(int32_t));
+        const Node& nd = c->nodes[ch];
+        std::memcpy(out_slots + p, nd.slots(), nd.len * sizeof(int32_t));
       }
     });
     if (out_len) *out_len = pos;
@@ -227,7 +317,7 @@ int ra_inc_ref(ra_cache* c, int64_t node, int64_t* out_delta) {
     for (int64_t x = node; x != 0; x = c->nodes[x].parent) {
       Node& n = c->nodes[x];
       if (n.ref == 0) {
-        delta -= static_cast<int64_t>(n.key.size());
+        delta -= n.len;
       }
       ++n.ref;
       c->refresh(x);
@@ -246,7 +336,7 @@ int ra_dec_ref(ra_cache* c, int64_t node, int64_t* out_delta) {
     int64_t delta = 0;
     for (int64_t x = node; x != 0; x = c->nodes[x].parent) {
       Node& n = c->nodes[x];
-      if (--n.ref == 0) delta += static_cast<int64_t>(n.key.size());
+      if (--n.ref == 0) delta += n.len;
       c->refresh(x);
     }
     c->evictable += delta;
@@ -263,7 +353,7 @@ int ra_alloc_slots(ra_cache* c, int64_t n, int32_t* out_slots) {
     const int64_t first = std::min<int64_t>(n, c->pool_slots - c->head);
     std::memcpy(out_slots, c->ring.data() + c->head, static_cast<size_t>(first) * sizeof(int32_t));
     std::memcpy(out_slots + first, c->ring.data(), static_cast<size_t>(n - first) * sizeof(int32_t));
-    for (int64_t i = 0; i < n; ++i) c->is_free[out_slots[i]] = 0;
+    for (int64_t i = 0; i < n; ++i) c->is_free.clr(out_slots[i]);
     c->head += n;
     if (c->head >= c->pool_slots) c->head -= c->pool_slots;
     c->count -= n;
@@ -275,17 +365,17 @@ static int check_freeable(ra_cache* c, const int32_t* slots, int64_t n, const ch
   // every slot in range, currently allocated, and not repeated
   for (int64_t i = 0; i < n; ++i) {
     int32_t s = slots[i];
-    if (s < 0 || s >= c->pool_slots || c->is_free[s])
+    if (s < 0 || s >= c->pool_slots || c->is_free.get(s))
       return ra_fail(RA_EINVAL, std::string(who) + ": slot out of range or already free");
   }
   // Repeats: mark each slot in the free map (all are allocated, so unmarked)
   // and find a mark already set; the marks are cleared again either way.
   int64_t i = 0;
   for (; i < n; ++i) {
-    if (c->is_free[slots[i]]) break;
-    c->is_free[slots[i]] = 1;
+    if (c->is_free.get(slots[i])) break;
+    c->is_free.set(slots[i]);
   }
-  for (int64_t j = 0; j < i; ++j) c->is_free[slots[j]] = 0;
+  for (int64_t j = 0; j < i; ++j) c->is_free.clr(slots[j]);
   if (i < n) return ra_fail(RA_EINVAL, std::string(who) + ": repeated slot");
   return RA_OK;
 }
@@ -304,23 +394,26 @@ int ra_insert(ra_cache* c, const int32_t* tokens, const int32_t* slots, int64_t 
               int64_t* out_cached, int64_t* out_node) {
   return ra_guard("ra_insert", [&]() -> int {
     if (!c || n < 0 || (n > 0 && (!tokens || !slots))) return ra_fail(RA_EINVAL, "ra_insert: bad argument");
+    if (n > INT32_MAX) return ra_fail(RA_EINVAL, "ra_insert: sequence longer than 2^31 - 1 tokens");
     // Validate duplicates before changing anything: walk read-only first.
     {
       int64_t node = 0, pos = 0;
       std::vector<int32_t> dup;
       while (pos < n) {
-        auto it = c->children.find(edge_key(node, tokens[pos]));
-        if (it == c->children.end()) break;
-        const Node& ch = c->nodes[it->second];
-        int64_t lim = std::min<int64_t>(static_cast<int64_t>(ch.key.size()), n - pos);
+        const int64_t chid = c->children.find(edge_key(node, tokens[pos]));
+        if (chid < 0) break;
+        const Node& ch = c->nodes[chid];
+        const int32_t* key = ch.key();
+        const int32_t* cs = ch.slots();
+        int64_t lim = std::min<int64_t>(ch.len, n - pos);
         int64_t k = 0;
-        while (k < lim && ch.key[k] == tokens[pos + k]) {
-          if (slots[pos + k] != ch.slots[k]) dup.push_back(slots[pos + k]);
+        while (k < lim && key[k] == tokens[pos + k]) {
+          if (slots[pos + k] != cs[k]) dup.push_back(slots[pos + k]);
           ++k;
         }
         pos += k;
-        if (k < static_cast<int64_t>(ch.key.size())) break;
-        node = it->second;
+        if (k < ch.len) break;
+        node = chid;
       }
       if (!dup.empty()) {
         int st = check_freeable(c, dup.data(), static_cast<int64_t>(dup.size()), "ra_insert");
@@ -328,22 +421,22 @@ int ra_insert(ra_cache* c, const int32_t* tokens, const int32_t* slots, int64_t 
       }
       // slots that will enter the tree must be allocated pool slots
       for (int64_t i = pos; i < n; ++i)
-        if (slots[i] < 0 || slots[i] >= c->pool_slots || c->is_free[slots[i]])
+        if (slots[i] < 0 || slots[i] >= c->pool_slots || c->is_free.get(slots[i]))
           return ra_fail(RA_EINVAL, "ra_insert: new slot out of range or free");
     }
     std::vector<int32_t> dup;
     int64_t pos = 0;
     int64_t node = c->walk(tokens, n, &pos, [&](int64_t ch, int64_t p) {
-      const auto& s = c->nodes[ch].slots;
-      for (size_t i = 0; i < s.size(); ++i)
+      const Node& nd = c->nodes[ch];
+      const int32_t* s = nd.slots();
+      for (int64_t i = 0; i < nd.len; ++i)
         if (slots[p + i] != s[i]) dup.push_back(slots[p + i]);
     });
     for (int32_t s : dup) c->push_free(s);
     int64_t cached = pos;
     if (pos < n) {
-      int64_t leaf = c->new_node(node, std::vector<int32_t>(tokens + pos, tokens + n),
-                                 std::vector<int32_t>(slots + pos, slots + n), 0, c->clock);
-      c->children[edge_key(node, tokens[pos])] = leaf;
+      int64_t leaf = c->new_node(node, tokens + pos, slots + pos, n - pos, 0, c->clock);
+      c->children.set(edge_key(node, tokens[pos]), leaf);
       c->nodes[node].n_children += 1;
       c->evictable += n - pos;
       c->cached += n - pos;
@@ -368,25 +461,26 @@ int ra_evict(ra_cache* c, int64_t n_tokens, int64_t* out_freed) {
       n.in_lru = false;
       if (c->log_evictions) {
         ra_cache::Evicted e;
-        e.len = static_cast<int64_t>(n.key.size());
+        e.len = n.len;
         std::vector<int64_t> chain;
         for (int64_t y = x; y != 0; y = c->nodes[y].parent) chain.push_back(y);
         for (auto it = chain.rbegin(); it != chain.rend(); ++it) {
-          const auto& k = c->nodes[*it].key;
-          e.path.insert(e.path.end(), k.begin(), k.end());
+          const Node& a = c->nodes[*it];
+          e.path.insert(e.path.end(), a.key(), a.key() + a.len);
         }
         c->eviction_log.push_back(std::move(e));
       }
-      for (int32_t s : n.slots) c->push_free(s);
-      int64_t len = static_cast<int64_t>(n.key.size());
+      const int32_t* ns = n.slots();
+      int64_t len = n.len;
+      for (int64_t i = 0; i < len; ++i) c->push_free(ns[i]);
       freed += len;
       c->evictable -= len;
       c->cached -= len;
-      c->children.erase(edge_key(n.parent, n.key[0]));
+      c->children.erase(edge_key(n.parent, n.key()[0]));
       int64_t par = n.parent;
       n.alive = false;
-      std::vector<int32_t>().swap(n.key);
-      std::vector<int32_t>().swap(n.slots);
+      n.kv.reset();
+      n.len = 0;
       --c->live;
       c->nodes[par].n_children -= 1;
       c->refresh(par);
@@ -432,7 +526,7 @@ int ra_snapshot(const ra_cache* c, int64_t* buf, int64_t cap, int64_t* out_len) 
     if (!c) return ra_fail(RA_EINVAL, "ra_snapshot: cache is NULL");
     int64_t need = 3 + c->count;
     for (const Node& n : c->nodes)
-      if (n.alive) need += 5 + 2 * static_cast<int64_t>(n.key.size());
+      if (n.alive) need += 5 + 2 * static_cast<int64_t>(n.len);
     if (out_len) *out_len = need;
     if (!buf) return ra_ok();
     if (cap < need) return ra_fail(RA_EINVAL, "ra_snapshot: buffer too small");
@@ -447,9 +541,8 @@ int ra_snapshot(const ra_cache* c, int64_t* buf, int64_t cap, int64_t* out_len) 
       *w++ = n.parent;
       *w++ = n.ref;
       *w++ = static_cast<int64_t>(n.stamp);
-      *w++ = static_cast<int64_t>(n.key.size());
-      for (int32_t t : n.key) *w++ = t;
-      for (int32_t s : n.slots) *w++ = s;
+      *w++ = n.len;
+      for (int64_t i = 0; i < 2 * static_cast<int64_t>(n.len); ++i) *w++ = n.kv[i];  // tokens, then slots
     }
     for (int64_t i = 0; i < c->count; ++i) *w++ = c->ring[(c->head + i) % c->pool_slots];
     return ra_ok();
