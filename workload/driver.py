@@ -48,6 +48,8 @@ class PhaseInputs:
     new_slots: torch.Tensor  # [sum E + B_dec] int32
     ext_meta: list           # (tokens, P, E, start row)
     dec_meta: list           # (tokens, L)
+    table_host: np.ndarray   # host copies of table and rpi (the scheduler builds them on the host)
+    rpi_host: np.ndarray
 
 
 class ScenarioRun:
@@ -138,7 +140,8 @@ class ScenarioRun:
             extend_start=dt(starts), seq_lens=dt([l for _, l in dec]),
             max_extend_len=max([e for _, _, e in ext], default=0), max_seq_len=max([l for _, l in dec], default=0),
             total_ext=total_ext, q_ext=q_ext, q_dec=q_dec, k_new=k_new, v_new=v_new,
-            new_slots=dt(new_slots), ext_meta=ext_meta, dec_meta=dec)
+            new_slots=dt(new_slots), ext_meta=ext_meta, dec_meta=dec, table_host=np.ascontiguousarray(table, dtype=np.int32),
+            rpi_host=np.ascontiguousarray(rpi, dtype=np.int32))
 
     # -- the hot path ----------------------------------------------------------
     def store(self, inp: PhaseInputs) -> None:
@@ -185,9 +188,9 @@ class ScenarioRun:
             cus = torch.cuda.get_device_properties(0).multi_processor_count if torch.cuda.is_available() else 256
             min_items = -(-4 * cus // self.sc.hkv)
         t0 = time.perf_counter()
-        plan = pa.ra_decode_share_plan(inp.table.cpu().numpy(), inp.rpi[inp.n_ext:].cpu().numpy(),
-                                       inp.seq_lens.cpu().numpy(), members_per_item, min_shared, chunk_len,
-                                       min_items)
+        lens = np.array([l for _, l in inp.dec_meta], dtype=np.int32)
+        plan = pa.ra_decode_share_plan(inp.table_host, inp.rpi_host[inp.n_ext:], lens, members_per_item, min_shared,
+                                       chunk_len, min_items)
         self.share_plan_seconds = time.perf_counter() - t0
         return plan, torch.from_numpy(plan.words).to(self.device)
 
