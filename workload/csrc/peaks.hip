@@ -1,7 +1,8 @@
 // Machine-peak microbenchmarks for the roofline report (bench.py --peaks):
 // the HBM read bandwidth a streaming kernel reaches, the bandwidth of random
 // 256-byte row gathers (the access pattern of attention over a pool of
-// one-token pages), and the bf16 rate of a loop of matrix-core instructions.
+// one-token pages, also in the decode kernels' own tile pattern), and the
+// bf16 rate of a loop of matrix-core instructions.
 // They compute no attention; each folds what it reads into one word per
 // thread so the compiler keeps every load.
 #include <hip/hip_runtime.h>
@@ -60,6 +61,57 @@ __global__ __launch_bounds__(256) void pk_gather_kernel(const unsigned char* __r
   sink[static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x] = acc;
 }
 
+// Gather in the decode kernels' own pattern: 32-row tiles of one head's K row
+// and V row (256 bytes each, two pools of slot_bytes-byte slots), each wave
+// instruction reading 64 bytes of 16 rows (lane: row lane & 15 of a 16-row
+// half, 16-byte piece lane >> 4 of a 64-byte quarter); a tile is 8 K and 8 V
+// instructions (16 KB), two tiles in flight per wave, one wave per SIMD.  The
+// slot indices of a tile (one per lane of the first 32) are loaded two tiles
+// ahead, after the loads of the tile before, and spread with a lane shuffle.
+// Wave w walks tiles w * tiles .. w * tiles + tiles - 1 of the row list.
+__global__ __launch_bounds__(256) void pk_gather_kv_kernel(const unsigned char* __restrict__ kpool,
+                                                           const unsigned char* __restrict__ vpool,
+                                                           const int32_t* __restrict__ slots, int32_t tiles,
+                                                           int32_t slot_bytes, uint32_t* __restrict__ sink) {
+  const int lane = threadIdx.x & 63;
+  const int64_t wave = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
+  const int head = static_cast<int>(wave & 7);
+  uint4 kb[2][2][4], vb[2][2][4];
+  int32_t ib[2];
+  uint32_t acc = 0;
+  auto idx_of = [&](int t) { return slots[(wave * tiles + min(t, tiles - 1)) * 32 + (lane & 31)]; };
+  auto load = [&](int j, int32_t idx) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int64_t off = static_cast<int64_t>(__shfl(idx, (lane & 15) + 16 * h)) * slot_bytes + head * 256 +
+                          16 * (lane >> 4);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        kb[j][h][q] = *reinterpret_cast<const uint4*>(kpool + off + 64 * q);
+        vb[j][h][q] = *reinterpret_cast<const uint4*>(vpool + off + 64 * q);
+      }
+    }
+  };
+  ib[0] = idx_of(0);
+  ib[1] = idx_of(1);
+  load(0, ib[0]);
+  load(1, ib[1]);
+  ib[0] = idx_of(2);
+  ib[1] = idx_of(3);
+  for (int t = 0; t < tiles; t += 2) {
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) acc ^= pk_fold(kb[j][h][q]) ^ pk_fold(vb[j][h][q]);
+      if (t + j + 2 < tiles) load(j, ib[j]);
+      ib[j] = idx_of(t + j + 4);
+    }
+  }
+  sink[static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x] = acc;
+}
+
 // Matrix-core loop: eight independent accumulator chains per wave of bf16
 // MFMAs on register operands, one wave per SIMD (one 256-thread work-group
 // per CU), so each wave's cycles are its SIMD's.  SHAPE 16: 16x16x32
@@ -113,6 +165,15 @@ extern "C" int pk_gather(const void* pool, const int32_t* slots, int64_t n_rows,
                          void* sink, int32_t blocks, hipStream_t s) {
   hipLaunchKernelGGL(pk_gather_kernel, dim3(blocks), dim3(256), 0, s, static_cast<const unsigned char*>(pool), slots,
                      n_rows, heads, slot_bytes, static_cast<uint32_t*>(sink));
+  return hipGetLastError() == hipSuccess ? 0 : -3;
+}
+
+// tiles must be even; slots holds blocks * 4 * tiles * 32 entries in [0, pool rows).
+extern "C" int pk_gather_kv(const void* kpool, const void* vpool, const int32_t* slots, int32_t tiles,
+                            int32_t slot_bytes, void* sink, int32_t blocks, hipStream_t s) {
+  if (tiles < 2 || tiles % 2 != 0 || slot_bytes < 8 * 256) return -2;
+  hipLaunchKernelGGL(pk_gather_kv_kernel, dim3(blocks), dim3(256), 0, s, static_cast<const unsigned char*>(kpool),
+                     static_cast<const unsigned char*>(vpool), slots, tiles, slot_bytes, static_cast<uint32_t*>(sink));
   return hipGetLastError() == hipSuccess ? 0 : -3;
 }
 

@@ -4,6 +4,10 @@
 * ``gather256_gbs``: 16M random 256-byte head rows of an 8 GiB pool of
   2 KiB slots (8 heads x 128 x bf16), the access pattern of decode over a
   pool of one-token pages.
+* ``gather_kv_gbs``: the same rows read as the decode kernels read them:
+  K and V rows of one head from two 8 GiB pools in 32-row tiles, 64 bytes of
+  16 rows per wave instruction, two tiles in flight, one wave per SIMD
+  (8M random rows).
 * ``mfma16_bf16_tflops`` / ``mfma32_bf16_tflops``: loops of 16x16x32 and
   32x32x16 bf16 MFMAs, eight independent chains per wave, one wave per SIMD;
   with the cycles per instruction and the shader clock each wave measured.
@@ -28,8 +32,9 @@ def _lib():
     vp, i64, i32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32
     lib.pk_read.argtypes = [vp, i64, vp, i32, vp]
     lib.pk_gather.argtypes = [vp, vp, i64, i32, i32, vp, i32, vp]
+    lib.pk_gather_kv.argtypes = [vp, vp, vp, i32, i32, vp, i32, vp]
     lib.pk_mfma.argtypes = [i32, i32, vp, vp, i32, vp]
-    for f in (lib.pk_read, lib.pk_gather, lib.pk_mfma):
+    for f in (lib.pk_read, lib.pk_gather, lib.pk_gather_kv, lib.pk_mfma):
         f.restype = ctypes.c_int
     return lib
 
@@ -81,6 +86,17 @@ def measure(reps: int = 7, read_gib: int = 4, pool_gib: int = 8, gather_rows: in
                                             sink.data_ptr(), blocks, s.cuda_stream)), reps)
     out["gather256_gbs"] = gather_rows * 256 / (ms * 1e-3) / 1e9
     del pool, slots
+
+    # decode tile pattern: one 256-thread work-group per CU, 64 tiles of 32 rows per wave
+    kv_blocks, kv_tiles = cus, 64
+    kv_rows = kv_blocks * 4 * kv_tiles * 32
+    kpool = torch.ones((pool_gib << 30) // 4, dtype=torch.int32, device=dev)
+    vpool = torch.ones((pool_gib << 30) // 4, dtype=torch.int32, device=dev)
+    slots = torch.from_numpy(np.random.default_rng(1).integers(0, n_slots, kv_rows, dtype=np.int32)).to(dev)
+    ms = _timed(lambda s: chk(lib.pk_gather_kv(kpool.data_ptr(), vpool.data_ptr(), slots.data_ptr(), kv_tiles,
+                                               slot_bytes, sink.data_ptr(), kv_blocks, s.cuda_stream)), reps)
+    out["gather_kv_gbs"] = kv_rows * 512 / (ms * 1e-3) / 1e9
+    del kpool, vpool, slots
 
     mblocks = cus  # one 256-thread work-group per CU: one wave per SIMD
     fsink = torch.empty(mblocks * 256, dtype=torch.float32, device=dev)
