@@ -143,3 +143,33 @@ def test_scenario_tables_bit_exact(name):
         assert [list(r) for r in t.rows] == [r.tolist() for r in p.rows]
         assert t.new_ctx == p.new_ctx and t.matched == p.matched and t.locks == p.locks
     assert rp.tree.snapshot() == sch.cache.snapshot()
+
+
+@pytest.mark.parametrize("seed", range(2))
+def test_large_tree_bit_exact(seed):
+    """Trees of thousands of edges (the child-edge table grows past its first
+    sizes and deletes entries inside long probe runs on eviction), with many
+    requests ending inside shared edges: match results after every call and
+    whole-tree snapshots every 250 operations equal the oracle's."""
+    rng = np.random.default_rng(7000 + seed)
+    pool = 6000
+    o, n = _both(pool, rng.permutation(pool).astype(np.int32))
+    stems = [[int(x) for x in rng.integers(0, 40, size=int(rng.integers(20, 200)))] for _ in range(12)]
+    for step in range(2500):
+        stem = stems[int(rng.integers(len(stems)))]
+        seq = stem[: int(rng.integers(1, len(stem) + 1))] + [int(x) for x in rng.integers(0, 40, size=int(rng.integers(0, 12)))]
+        nid, m, slots = o.match_prefix(seq)
+        b = n.match_prefix(seq)
+        assert (nid, m, list(slots)) == (b[0], b[1], b[2].tolist())
+        need = len(seq) - m
+        if need > o.available_size():
+            k = need + int(rng.integers(0, 64))
+            assert o.evict(k)[0] == n.evict(k)
+        if need <= o.available_size():
+            s_o = o.alloc(need)
+            assert s_o == n.alloc(need).tolist()
+            assert o.insert(seq, list(slots) + s_o) == n.insert(seq, list(slots) + s_o)
+        if step % 250 == 249:
+            assert o.snapshot() == n.snapshot()
+    assert o.snapshot() == n.snapshot()
+    assert n.num_nodes() > 1000
