@@ -453,7 +453,9 @@ def main():
         "kernels": kernels,
         "host_tree": {"calls": run.history_ops, "seconds": run.history_seconds,
                       "calls_per_s": run.history_ops / max(run.history_seconds, 1e-9),
-                      "plan_batch_ms": run.plan_seconds * 1e3},
+                      "plan_batch_ms": run.plan_seconds * 1e3,
+                      "plan_batch_requests": inp.n_ext + inp.n_dec,
+                      "plan_ms_per_request": run.plan_seconds * 1e3 / max(inp.n_ext + inp.n_dec, 1)},
     }
     line["scheduler"] = scheduler_report(sc)
     line["data_parallel"] = data_parallel_report(sc)
