@@ -275,7 +275,9 @@ int ra_decode_attention_noalloc(const void* q, const void* k_pool, const void* v
  * worth of waves per SIMD divided by Hkv; the shortest if none does).
  *   req_to_token [rtt_rows, rtt_stride], req_pool_idx [B], seq_lens [B]:
  *          host copies of the arrays ra_decode_attention takes (L clamped to
- *          [0, rtt_stride]; requests with L = 0 get no item); RA_EINVAL for a
+ *          [0, rtt_stride]; a request with L = 0 gets no item and
+ *          ra_decode_attention_shared leaves its output rows as they were:
+ *          decode requires L >= 1); RA_EINVAL for a
  *          table row outside [0, rtt_rows)
  *   plan:  int32 output of plan_capacity words; *plan_len receives the
  *          length needed.  plan = NULL only queries the length; a shorter
