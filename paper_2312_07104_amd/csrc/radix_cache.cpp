@@ -61,10 +61,11 @@ inline uint64_t edge_key(int64_t parent, int32_t tok) {
   return (static_cast<uint64_t>(parent) << 32) ^ static_cast<uint32_t>(tok);
 }
 
-
 // Open-addressing map from edge key to child id: linear probing over a
 // power-of-two table at most 3/4 full, deletion by backward shift (no
-// tombstones).  The slot hash is the 64-bit finalizer of MurmurHash3.
+// tombstones).  The slot hash is the first xor-shift-multiply round of
+// MurmurHash3's 64-bit finalizer.  Keys are below 2^63 (node ids < 2^31), so
+// the all-ones word marks an empty entry.
 class EdgeMap {
  public:
   EdgeMap() { rehash(1024); }
