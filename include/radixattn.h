@@ -22,7 +22,8 @@
  *     bf16 rounding.
  *
  * Conventions.  Tokens and slots are int32 (S < 2^31).  Host lengths are
- * int64.  Node handles are int64 ids; the root is 0; ids are never reused.
+ * int64.  Node handles are int64 ids; the root is 0; ids are never reused
+ * (after 2^31 - 1 nodes a match or insert returns RA_ENOMEM, no effect).
  * Every call returns RA_OK or a negative status and never throws; the text of
  * the last error on the calling thread is available from ra_last_error().  A
  * failing call changes nothing, with one exception: when the host runs out of

@@ -290,10 +290,18 @@ int ra_cache_create(int64_t pool_slots, const int32_t* order, ra_cache** out) {
 
 void ra_cache_destroy(ra_cache* c) { delete c; }
 
+// A match creates at most one node (a split) and an insert at most two (a
+// split and the new leaf); ids stay below 2^31, which the child table's keys
+// rely on.
+static bool ids_left(const ra_cache* c, int64_t need) {
+  return static_cast<int64_t>(c->nodes.size()) + need <= INT32_MAX;
+}
+
 int ra_match_prefix(ra_cache* c, const int32_t* tokens, int64_t n, int32_t* out_slots,
                     int64_t* out_len, int64_t* out_node) {
   return ra_guard("ra_match_prefix", [&]() -> int {
     if (!c || n < 0 || (n > 0 && !tokens)) return ra_fail(RA_EINVAL, "ra_match_prefix: bad argument");
+    if (!ids_left(c, 1)) return ra_fail(RA_ENOMEM, "ra_match_prefix: node ids exhausted (2^31 created)");
     int64_t pos = 0;
     int64_t node = c->walk(tokens, n, &pos, [&](int64_t ch, int64_t p) {
       if (out_slots) {
@@ -396,6 +404,7 @@ int ra_insert(ra_cache* c, const int32_t* tokens, const int32_t* slots, int64_t 
   return ra_guard("ra_insert", [&]() -> int {
     if (!c || n < 0 || (n > 0 && (!tokens || !slots))) return ra_fail(RA_EINVAL, "ra_insert: bad argument");
     if (n > INT32_MAX) return ra_fail(RA_EINVAL, "ra_insert: sequence longer than 2^31 - 1 tokens");
+    if (!ids_left(c, 2)) return ra_fail(RA_ENOMEM, "ra_insert: node ids exhausted (2^31 created)");
     // Validate duplicates before changing anything: walk read-only first.
     {
       int64_t node = 0, pos = 0;
