@@ -405,14 +405,23 @@ int ra_insert(ra_cache* c, const int32_t* tokens, const int32_t* slots, int64_t 
     if (!c || n < 0 || (n > 0 && (!tokens || !slots))) return ra_fail(RA_EINVAL, "ra_insert: bad argument");
     if (n > INT32_MAX) return ra_fail(RA_EINVAL, "ra_insert: sequence longer than 2^31 - 1 tokens");
     if (!ids_left(c, 2)) return ra_fail(RA_ENOMEM, "ra_insert: node ids exhausted (2^31 created)");
-    // Validate duplicates before changing anything: walk read-only first.
+    // One read-only walk records the path and the caller slots that differ
+    // from cached ones, and everything is validated before the tree changes;
+    // then the recorded path is stamped (and split where the match ends
+    // inside an edge) without walking again.
+    struct Step {
+      int64_t child, matched;
+    };
+    std::vector<Step> path;
+    std::vector<int32_t> dup;
+    int64_t pos = 0;
     {
-      int64_t node = 0, pos = 0;
-      std::vector<int32_t> dup;
+      int64_t node = 0;
       while (pos < n) {
         const int64_t chid = c->children.find(edge_key(node, tokens[pos]));
         if (chid < 0) break;
         const Node& ch = c->nodes[chid];
+        if (pos + ch.len < n) c->children.prefetch(edge_key(chid, tokens[pos + ch.len]));
         const int32_t* key = ch.key();
         const int32_t* cs = ch.slots();
         int64_t lim = std::min<int64_t>(ch.len, n - pos);
@@ -421,6 +430,7 @@ int ra_insert(ra_cache* c, const int32_t* tokens, const int32_t* slots, int64_t 
           if (slots[pos + k] != cs[k]) dup.push_back(slots[pos + k]);
           ++k;
         }
+        path.push_back({chid, k});
         pos += k;
         if (k < ch.len) break;
         node = chid;
@@ -434,14 +444,15 @@ int ra_insert(ra_cache* c, const int32_t* tokens, const int32_t* slots, int64_t 
         if (slots[i] < 0 || slots[i] >= c->pool_slots || c->is_free.get(slots[i]))
           return ra_fail(RA_EINVAL, "ra_insert: new slot out of range or free");
     }
-    std::vector<int32_t> dup;
-    int64_t pos = 0;
-    int64_t node = c->walk(tokens, n, &pos, [&](int64_t ch, int64_t p) {
-      const Node& nd = c->nodes[ch];
-      const int32_t* s = nd.slots();
-      for (int64_t i = 0; i < nd.len; ++i)
-        if (slots[p + i] != s[i]) dup.push_back(slots[p + i]);
-    });
+    ++c->clock;
+    int64_t node = 0;
+    for (const Step& st : path) {
+      int64_t ch = st.child;
+      if (st.matched < c->nodes[ch].len) ch = c->split(ch, st.matched);
+      c->nodes[ch].stamp = c->clock;
+      c->refresh(ch);
+      node = ch;
+    }
     for (int32_t s : dup) c->push_free(s);
     int64_t cached = pos;
     if (pos < n) {
