@@ -225,3 +225,28 @@ def test_mixed_shared_call_equals_separate_calls():
             run.k_pool, run.v_pool, inp.table, sc.scale, out_ext=sentinel)
     torch.cuda.synchronize()
     assert bool((sentinel == 7.0).all())
+
+
+def test_mixed_shared_call_with_an_empty_half():
+    """ra_mixed_attention_shared with no extend tokens runs only the shared
+    decode, and with no decode requests (the plan of an empty batch) only the
+    extend: outputs equal the single calls bit for bit."""
+    sc = S.cfg5_mixed_small()
+    log(f"case: mixed shared call with an empty half seed={sc.seed}")
+    run, inp = _prep(sc)
+    plan, plan_dev = run.share_plan(inp, min_shared=16)
+    od = run.decode_shared(inp, plan, plan_dev)
+    oe = run.extend(inp)
+    z = torch.zeros(0, dtype=torch.int32, device="cuda")
+    _, md = pa.ra_mixed_attention_shared(
+        inp.q_ext[:0], inp.k_new[:0], inp.v_new[:0], z, z, z, z, 0, inp.q_dec, plan, plan_dev,
+        run.k_pool, run.v_pool, inp.table, sc.scale)
+    eplan = pa.ra_decode_share_plan(inp.table_host, np.zeros(0, np.int32), np.zeros(0, np.int32), 4)
+    assert eplan.n_items == 0
+    eplan_dev = torch.from_numpy(eplan.words).to("cuda")
+    me, _ = pa.ra_mixed_attention_shared(
+        inp.q_ext, inp.k_new[: inp.total_ext], inp.v_new[: inp.total_ext], inp.rpi[: inp.n_ext], inp.prefix_lens,
+        inp.extend_lens, inp.extend_start, inp.max_extend_len, inp.q_dec[:0], eplan, eplan_dev,
+        run.k_pool, run.v_pool, inp.table, sc.scale)
+    torch.cuda.synchronize()
+    assert torch.equal(md, od) and torch.equal(me, oe)
